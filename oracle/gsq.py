@@ -1,0 +1,421 @@
+"""Plain CPU oracle of one GSQ layer: init, relaxed step, hardening.  Test infrastructure only.
+
+Written from the paper (Gumbel-Softmax Quantization, arXiv 2604.18556), in
+float64 unless a storage precision is part of the path:
+
+* the optimiser state (logits, moments, scales) is stored in float32;
+* the noise g is float32 (the generator's output, see ``oracle.philox``);
+* in the "bf16" precision the residual R and H enter the contraction rounded to
+  bfloat16 (round-to-nearest-even), as the kernel's inputs are; the
+  contraction itself is accumulated in float64 here;
+* in the "fp32" precision R and H enter the contraction as float32 values.
+
+Notation (the paper's where it has one): W is O x I, groups of ``gs``
+consecutive inputs along a row share one scale s (§4.1 "Quantization
+configuration"); every coordinate carries K logits over grid levels
+c_0 < ... < c_{K-1} (§3.2, Eq. 5); H = X^T X is the layer's calibration Gram
+matrix, so the reconstruction error of Eq. 1 for a linear layer is
+tr((W - W_hat) H (W - W_hat)^T).
+
+Readings where the paper is silent are listed in the design notes; each is
+repeated at the function that takes it.
+"""
+from dataclasses import dataclass, field
+
+import numpy as np
+
+from . import philox
+
+F32 = np.float32
+
+
+# ----------------------------------------------------------------------------- rounding helpers
+def round_f32(x):
+    """Round float64 values to float32 and back (exact representable values)."""
+    return np.asarray(x, dtype=np.float64).astype(np.float32).astype(np.float64)
+
+
+def round_bf16(x):
+    """Round to bfloat16 with round-to-nearest-even, returned as float64.
+
+    bfloat16 keeps the top 16 bits of an IEEE float32: the value is first
+    rounded to float32, then the low 16 bits are rounded away (ties to even).
+    NaN/Inf are not expected here.
+    """
+    b = np.asarray(x, dtype=np.float64).astype(np.float32).view(np.uint32).astype(np.uint64)
+    lsb = (b >> np.uint64(16)) & np.uint64(1)
+    b = (b + np.uint64(0x7FFF) + lsb) & np.uint64(0xFFFF0000)
+    return b.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+def to_contraction_precision(cfg, x):
+    """Round an operand of the contraction to the path's storage type.
+
+    "bf16": bfloat16 (RNE); "fp32": float32; "fp64": unrounded (used only by the
+    mathematical pins, e.g. finite differences).
+    """
+    if cfg.precision == "bf16":
+        return round_bf16(x)
+    if cfg.precision == "fp32":
+        return round_f32(x)
+    return np.asarray(x, np.float64)
+
+
+# ----------------------------------------------------------------------------- configuration
+@dataclass
+class Config:
+    """One layer (or a batch of independent layers, e.g. MoE experts)."""
+    out_features: int
+    in_features: int
+    levels: tuple                      # c_0 < ... < c_{K-1}
+    group_size: int = 128              # gs, along the input dimension (§4.1)
+    batch: int = 1
+    layout: str = "group"              # "group" | "superblock"
+    precision: str = "fp32"            # "fp32" | "bf16" | "fp64": dtype of R and H in the contraction
+    seed: int = 0
+    alpha: float = 6.0                 # warm-start strength of Eq. 4 (Tab. 7: 6 for 2/3-bit)
+    sigma_init: float = 1.0            # overall logit scale of Eq. 4
+    init_noise: bool = True
+
+    @property
+    def K(self):
+        return len(self.levels)
+
+    @property
+    def gs(self):
+        return 16 if self.layout == "superblock" else self.group_size
+
+    def levels64(self):
+        return np.asarray(self.levels, dtype=np.float32).astype(np.float64)
+
+
+@dataclass
+class StepParams:
+    tau: float
+    kappa: float = 1.0
+    lr_logits: float = 1e-2
+    lr_scales: float = 5e-5
+    beta1: float = 0.9
+    beta2: float = 0.95
+    eps: float = 1e-8
+    gumbel_noise: bool = True
+
+
+def as_f32_params(prm):
+    """The step's scalars as the float32 values the library receives."""
+    f = lambda x: float(np.float32(x))
+    return StepParams(f(prm.tau), f(prm.kappa), f(prm.lr_logits), f(prm.lr_scales),
+                      f(prm.beta1), f(prm.beta2), f(prm.eps), bool(prm.gumbel_noise))
+
+
+@dataclass
+class State:
+    """Optimiser state of one layer, float32 storage (logits in O x I x K order)."""
+    logits: np.ndarray                 # (B, O, I, K) float32
+    m: np.ndarray
+    v: np.ndarray
+    scales: np.ndarray                 # (B, O, I // gs) float32
+    m_s: np.ndarray
+    v_s: np.ndarray
+    t: int = 0
+    sb_d: np.ndarray = None            # super-block fp16 d, (B, O, I // 256)
+    sb_sc: np.ndarray = None           # super-block 6-bit sub-scales, (B, O, I // 16)
+    extra: dict = field(default_factory=dict)
+
+    def copy(self):
+        c = State(self.logits.copy(), self.m.copy(), self.v.copy(), self.scales.copy(),
+                  self.m_s.copy(), self.v_s.copy(), self.t,
+                  None if self.sb_d is None else self.sb_d.copy(),
+                  None if self.sb_sc is None else self.sb_sc.copy())
+        return c
+
+
+# ----------------------------------------------------------------------------- initialisation
+def symmetrize(H):
+    """(H + H^T) / 2, rounded to float32.
+
+    The objective only sees the symmetric part of H (tr(R H R^T) = tr(R H^T R^T)),
+    so symmetrising changes nothing mathematically and makes the gradient
+    -2 R H exact (reading: the library symmetrises its copy of H).
+    """
+    H = np.asarray(H, dtype=np.float64)
+    return round_f32((H + np.swapaxes(H, -1, -2)) * 0.5)
+
+
+def group_absmax_scales(W, cfg):
+    """Initial group scales: s = max|W_group| / max_k |c_k| (float32 division).
+
+    The paper takes the initial scale from its warm start (GPTQ, Eq. 4's
+    paragraph); the warm start here is round-to-nearest, whose symmetric scale
+    maps the group's largest magnitude onto the outermost grid level.  An
+    all-zero group gets s = 1 (reading).
+    """
+    B, O, I = W.shape
+    gs = cfg.group_size
+    absmax = np.abs(W.reshape(B, O, I // gs, gs)).max(axis=-1).astype(np.float32)
+    cmax = np.float32(np.abs(cfg.levels64()).max())
+    s = absmax / cmax                                   # IEEE float32 division
+    s[s == 0] = 1.0
+    return s.astype(np.float32)
+
+
+def superblock_scales(W, cfg):
+    """K-quant-style scales: 256-weight super-blocks of 16 sub-blocks of 16.
+
+    Each sub-block j has a raw absmax scale s_j = max|W_j| / max|c|; the
+    super-block stores d = fp16(max_j s_j / 63) and 6-bit integers
+    sc_j = clamp(rint(s_j / d), 0, 63), and the effective scale is d * sc_j
+    (§4.4 and App. E keep the optimised weights in the deployment format; the
+    byte layout is ours).  Returns (d fp16 (B,O,I/256), sc uint8 (B,O,I/16),
+    effective float32 scales (B,O,I/16)).
+    """
+    B, O, I = W.shape
+    cmax = np.float32(np.abs(cfg.levels64()).max())
+    absmax = np.abs(W.reshape(B, O, I // 16, 16)).max(axis=-1).astype(np.float32)
+    raw = (absmax / cmax).astype(np.float32)
+    per_sb = raw.reshape(B, O, I // 256, 16)
+    d = (per_sb.max(axis=-1) / np.float32(63.0)).astype(np.float32).astype(np.float16)
+    d32 = d.astype(np.float32)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        q = np.where(d32[..., None] > 0, per_sb / d32[..., None], np.float32(0)).astype(np.float32)
+    sc = np.clip(np.rint(q), 0, 63).astype(np.uint8)
+    eff = (d32[..., None] * sc.astype(np.float32)).astype(np.float32)
+    return d, sc.reshape(B, O, I // 16), eff.reshape(B, O, I // 16)
+
+
+def expand_scales(scales, gs):
+    """Per-coordinate view of group scales: (B, O, I/gs) -> (B, O, I)."""
+    return np.repeat(scales, gs, axis=-1)
+
+
+def rtn_codes(W, s_coord, cfg):
+    """Round-to-nearest level index q0 = argmin_k |fl32(W / s) - c_k|, ties to the lower k.
+
+    The ratio is taken in float32 (IEEE division); distances to the levels are
+    exact.  A zero scale (an all-zero super-block sub-block) uses ratio 0.
+    """
+    c = cfg.levels64()
+    W32 = np.asarray(W, dtype=np.float32)
+    s32 = np.asarray(s_coord, dtype=np.float32)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        u = np.where(s32 != 0, W32 / s32, np.float32(0)).astype(np.float64)
+    dist = np.abs(u[..., None] - c)                     # exact in float64
+    return np.argmin(dist, axis=-1)                      # first minimum = lower index
+
+
+def prior_logits(q0, cfg):
+    """Gaussian-prior warm-start logits (App. A), mean-subtracted per coordinate.
+
+    l_k = -(c_k - mu)^2 / 2 with mu = c_{q0}, then the mean over k is removed.
+    """
+    c = cfg.levels64()
+    mu = c[q0][..., None]
+    l = -0.5 * (c - mu) ** 2
+    return l - l.mean(axis=-1, keepdims=True)
+
+
+def init_logits(q0, cfg, eps=None):
+    """Eq. 4: l = sigma_init * (eps + alpha * l_prior); eps ~ N(0, I) or zero."""
+    lp = prior_logits(q0, cfg)
+    noise = 0.0 if eps is None else eps
+    return round_f32(cfg.sigma_init * (noise + cfg.alpha * lp)).astype(np.float32)
+
+
+def coord_index(cfg, b, rows):
+    """Global coordinate indices e = (b*O + o)*I + i for the given rows of layer b."""
+    rows = np.asarray(rows, dtype=np.int64)
+    i = np.arange(cfg.in_features, dtype=np.int64)
+    return ((b * cfg.out_features + rows)[:, None] * cfg.in_features + i[None, :]).reshape(-1)
+
+
+def init_layer(cfg, W, scales_init=None):
+    """Initial state of ``gsq_layer_init``: scales, RTN codes, logits, zero moments."""
+    W = np.asarray(W, dtype=np.float64).reshape(cfg.batch, cfg.out_features, cfg.in_features)
+    B, O, I, K = cfg.batch, cfg.out_features, cfg.in_features, cfg.K
+    sb_d = sb_sc = None
+    if cfg.layout == "superblock":
+        sb_d, sb_sc, scales = superblock_scales(W, cfg)
+    elif scales_init is not None:
+        scales = np.asarray(scales_init, dtype=np.float32).reshape(B, O, I // cfg.gs).copy()
+    else:
+        scales = group_absmax_scales(W, cfg)
+    q0 = rtn_codes(W, expand_scales(scales, cfg.gs), cfg)
+    logits = np.empty((B, O, I, K), dtype=np.float32)
+    for b in range(B):
+        eps = None
+        if cfg.init_noise:
+            e = coord_index(cfg, b, np.arange(O))
+            eps = philox.init_normals(cfg.seed, e, K).reshape(O, I, K)
+        logits[b] = init_logits(q0[b], cfg, eps)
+    z = np.zeros_like(logits)
+    zs = np.zeros_like(scales)
+    st = State(logits, z, z.copy(), scales.astype(np.float32), zs, zs.copy(), 0, sb_d, sb_sc)
+    st.extra["q0"] = q0
+    return st
+
+
+# ----------------------------------------------------------------------------- one step
+def soft_sample(logits, g, tau, kappa):
+    """Alg. 1: p_k = exp((kappa l_k + g_k)/tau) / sum_j exp((kappa l_j + g_j)/tau).
+
+    Evaluated in float64 with the maximum subtracted first (the same quotient).
+    """
+    a = (kappa * np.asarray(logits, np.float64) + g) / np.float64(tau)
+    a = a - a.max(axis=-1, keepdims=True)
+    e = np.exp(a)
+    return e / e.sum(axis=-1, keepdims=True)
+
+
+def forward(cfg, W, logits, s_coord, g, tau, kappa):
+    """Soft weight and residual of one sample (Alg. 1 return value, scaled per §3.2).
+
+    v = sum_k p_k c_k, W_hat = s * v, R = W - W_hat.  Returns (p, v, R) where R
+    is rounded to the contraction's input precision.
+    """
+    p = soft_sample(logits, g, tau, kappa)
+    v = (p * cfg.levels64()).sum(axis=-1)
+    R = np.asarray(W, np.float64) - np.asarray(s_coord, np.float64) * v
+    return p, v, to_contraction_precision(cfg, R)
+
+
+def contract(cfg, R, Hs):
+    """P = R H and the loss L = sum(R * P) = tr(R H R^T) (Eq. 1 for a linear layer).
+
+    ``Hs`` is the symmetrised float32 H; in the bf16 precision it is rounded to
+    bfloat16 first.  Accumulation is float64.
+    """
+    Hc = to_contraction_precision(cfg, Hs)
+    P = R @ Hc
+    return P, float((R * P).sum())
+
+
+def backward(cfg, G, s_coord, p, v, tau, kappa):
+    """Gradients of L with respect to the logits and the group scales.
+
+    With W_hat = s v and G = dL/dW_hat:
+      dL/dl_k = G s (kappa / tau) p_k (c_k - v)         (softmax Jacobian, App. B proof)
+      dL/ds_g = sum_{i in g} G_i v_i
+    c_k - v is evaluated as sum_j p_j (c_k - c_j), equal because the p_j sum to
+    one; the direct difference cancels to rounding noise once one level holds
+    almost all the mass, which is the saturated regime App. B is about.
+    """
+    c = cfg.levels64()
+    diff = (p[..., None, :] * (c[:, None] - c[None, :])).sum(axis=-1)    # [.., k] = sum_j p_j (c_k - c_j)
+    dlog = (G * s_coord * (kappa / np.float64(tau)))[..., None] * p * diff
+    gv = G * v
+    B, O, I = gv.shape
+    dscale = gv.reshape(B, O, I // cfg.gs, cfg.gs).sum(axis=-1)
+    return dlog, dscale
+
+
+def adam(theta, m, v, grad, lr, beta1, beta2, eps, n):
+    """Adam (Kingma & Ba, 2015), bias-corrected at step n >= 1, no weight decay.
+
+    The paper's optimiser is Lion (§3.3); Adam is the variant this path builds.
+    Arithmetic in float64 on the float32 state; results stored as float32.
+    """
+    th = np.asarray(theta, np.float64)
+    m1 = beta1 * np.asarray(m, np.float64) + (1.0 - beta1) * grad
+    v1 = beta2 * np.asarray(v, np.float64) + (1.0 - beta2) * grad * grad
+    mhat = m1 / (1.0 - beta1 ** n)
+    vhat = v1 / (1.0 - beta2 ** n)
+    th1 = th - lr * mhat / (np.sqrt(vhat) + eps)
+    return th1.astype(np.float32), m1.astype(np.float32), v1.astype(np.float32)
+
+
+def step(cfg, W, Hs, st, prm, rows=None, want=False):
+    """One GSQ optimisation step on state ``st`` (returns a new state, the loss).
+
+    Order: noise -> soft sample -> residual -> contraction and loss -> gradient
+    -> Adam on logits and (if lr_scales > 0) scales; t -> t + 1.  The loss is
+    the one of this step's sample, before the update.
+
+    ``rows`` restricts the step to a subset of the rows of every layer (rows
+    are independent given H); noise indices stay the global ones.
+    ``want`` returns the intermediates (g, p, v, R, G, dlogits, dscales).
+    """
+    B, O, I, K = cfg.batch, cfg.out_features, cfg.in_features, cfg.K
+    prm = as_f32_params(prm)
+    rows = np.arange(O) if rows is None else np.asarray(rows)
+    W = np.asarray(W, np.float64).reshape(B, O, I)[:, rows]
+    Hs = np.asarray(Hs).reshape(B, I, I)
+    n = st.t + 1
+    new = st.copy()
+    losses = np.zeros(B)
+    inter = {k: [] for k in ("g", "p", "v", "R", "G", "dlogits", "dscales")}
+    for b in range(B):
+        e = coord_index(cfg, b, rows)
+        if prm.gumbel_noise:
+            g = philox.gumbel(cfg.seed, e, st.t, K).reshape(len(rows), I, K)
+        else:
+            g = np.zeros((len(rows), I, K))
+        lg = st.logits[b, rows]
+        sc = st.scales[b, rows]
+        s_coord = expand_scales(sc, cfg.gs)
+        p, v, R = forward(cfg, W[b], lg, s_coord, g, prm.tau, prm.kappa)
+        P, L = contract(cfg, R, Hs[b])
+        G = -2.0 * P
+        dlog, dsc = backward(cfg, G[None], s_coord[None], p[None], v[None], prm.tau, prm.kappa)
+        dlog, dsc = dlog[0], dsc[0]
+        losses[b] = L
+        th, m1, v1 = adam(lg, st.m[b, rows], st.v[b, rows], dlog, prm.lr_logits,
+                          prm.beta1, prm.beta2, prm.eps, n)
+        new.logits[b, rows], new.m[b, rows], new.v[b, rows] = th, m1, v1
+        if prm.lr_scales > 0:
+            ts, ms, vs = adam(sc, st.m_s[b, rows], st.v_s[b, rows], dsc, prm.lr_scales,
+                              prm.beta1, prm.beta2, prm.eps, n)
+            new.scales[b, rows], new.m_s[b, rows], new.v_s[b, rows] = ts, ms, vs
+        if want:
+            for k, val in zip(inter, (g, p, v, R, G, dlog, dsc)):
+                inter[k].append(val)
+    new.t = st.t + 1
+    if want:
+        return new, losses, {k: np.stack(v) for k, v in inter.items()}
+    return new, losses
+
+
+# ----------------------------------------------------------------------------- hardening
+def harden(logits):
+    """Hard codes q = argmax_k l_k, ties to the lowest k (the final step of Alg. 2, K-way)."""
+    return np.argmax(np.asarray(logits), axis=-1).astype(np.uint8)
+
+
+def scales_fp16(scales):
+    """Deployment scales: float32 -> float16, round-to-nearest-even (16-bit scales of Tab. 1)."""
+    return np.asarray(scales, dtype=np.float32).astype(np.float16)
+
+
+def hard_weights(cfg, codes, scales_eff):
+    """W_q = s * c[q] with the stored effective scales (float32 product)."""
+    c = np.asarray(cfg.levels, dtype=np.float32)
+    s = expand_scales(np.asarray(scales_eff, np.float32), cfg.gs)
+    return (s * c[codes]).astype(np.float32)
+
+
+def hard_loss(cfg, W, Hs, codes, scales_eff):
+    """Eq. 1 at the hardened weights: tr(R H R^T) with R = W - s c[q] (contraction precision)."""
+    W = np.asarray(W, np.float64).reshape(cfg.batch, cfg.out_features, cfg.in_features)
+    Hs = np.asarray(Hs).reshape(cfg.batch, cfg.in_features, cfg.in_features)
+    Wq = hard_weights(cfg, codes, scales_eff).astype(np.float64)
+    out = np.zeros(cfg.batch)
+    for b in range(cfg.batch):
+        R = to_contraction_precision(cfg, W[b] - Wq[b])
+        out[b] = contract(cfg, R, Hs[b])[1]
+    return out
+
+
+def harden_layer(cfg, W, Hs, st):
+    """``gsq_harden``: codes, effective scales (fp16-rounded in the plain layout), hard loss."""
+    codes = harden(st.logits)
+    if cfg.layout == "superblock":
+        eff = st.scales.astype(np.float32)
+    else:
+        eff = scales_fp16(st.scales).astype(np.float32)
+    return codes, eff, hard_loss(cfg, W, Hs, codes, eff)
+
+
+def tau_schedule(t, T, tau0=1.0, tau1=0.05):
+    """Linear temperature schedule (Tab. 7 anneals tau linearly); last step uses tau1."""
+    if T <= 1:
+        return tau1
+    return tau0 + (tau1 - tau0) * t / (T - 1)

@@ -1,0 +1,84 @@
+"""Pins of the oracle's generator: Philox4x32-10, the uniform map, Gumbel and normal noise."""
+import subprocess
+
+import numpy as np
+import pytest
+from scipy import stats
+
+from oracle import philox
+
+EULER_GAMMA = 0.5772156649015329
+
+
+def test_philox_matches_rocrand_host_implementation(rocrand_philox):
+    """Philox4x32-10 equals rocRAND's independent implementation on random keys/counters."""
+    rng = np.random.default_rng(5)
+    words = rng.integers(0, 2**32, size=(3000, 6), dtype=np.uint64)
+    words[:4] = [[0] * 6, [0xFFFFFFFF] * 6, [1, 0, 0, 0, 0, 0], [0, 0, 0, 0, 0, 1]]
+    text = "\n".join(" ".join(f"{int(x):x}" for x in row) for row in words) + "\n"
+    out = subprocess.run([rocrand_philox], input=text, capture_output=True, text=True, check=True)
+    ref = np.array([[int(x, 16) for x in line.split()] for line in out.stdout.strip().splitlines()],
+                   dtype=np.uint64)
+    key = (words[:, 0] | (words[:, 1] << np.uint64(32)))
+    got = np.empty_like(ref)
+    for n in range(len(words)):
+        r = philox.philox4x32_10(words[n, 2], words[n, 3], words[n, 4], words[n, 5], int(key[n]))
+        got[n] = [int(x) for x in r]
+    np.testing.assert_array_equal(got, ref)
+
+
+def test_counter_layout_fields_all_reach_the_output():
+    """Changing any of (e low, e high, t, stream, level block, seed) changes every output word."""
+    base = philox.raw_words(7, np.array([5], np.int64), 3, 0, 8)
+    for other in (philox.raw_words(7, np.array([6], np.int64), 3, 0, 8),
+                  philox.raw_words(7, np.array([5 + 2**32], np.int64), 3, 0, 8),
+                  philox.raw_words(7, np.array([5], np.int64), 4, 0, 8),
+                  philox.raw_words(7, np.array([5], np.int64), 3, 1, 8),
+                  philox.raw_words(8, np.array([5], np.int64), 3, 0, 8),
+                  philox.raw_words(7 + 2**32, np.array([5], np.int64), 3, 0, 8)):
+        assert np.all(other != base)
+    # levels 4..7 come from block j = 1, not from a shifted copy of block 0
+    assert np.all(base[0, 4:] != base[0, :4])
+
+
+def test_uniform_map_is_exact_and_uniform():
+    w = np.array([0, 1, 511, 512, 2**32 - 1], dtype=np.uint32)
+    u = philox.uniform(w)
+    assert u[0] == 2.0**-24 and u[-1] == 1 - 2.0**-24
+    assert u[1] == u[0] and u[3] == 3 * 2.0**-24
+    assert np.all(u.astype(np.float32).astype(np.float64) == u)
+    words = philox.raw_words(1, np.arange(250_000, dtype=np.int64), 0, 0, 4).reshape(-1)
+    counts = np.bincount(words >> np.uint32(24), minlength=256)
+    assert stats.chisquare(counts).pvalue > 1e-4
+
+
+def test_gumbel_moments():
+    """Gumbel(0,1): mean = Euler-Mascheroni constant, variance = pi^2 / 6."""
+    g = philox.gumbel(3, np.arange(500_000, dtype=np.int64), 11, 4).reshape(-1)
+    n = g.size
+    var = np.pi**2 / 6
+    assert abs(g.mean() - EULER_GAMMA) < 5 * np.sqrt(var / n)
+    # variance of the sample variance for Gumbel: (mu4 - sigma^4)/n with excess kurtosis 12/5
+    mu4 = (3 + 12 / 5) * var**2
+    assert abs(g.var() - var) < 5 * np.sqrt((mu4 - var**2) / n)
+    assert stats.kstest(g[:200_000], stats.gumbel_r.cdf).pvalue > 1e-4
+
+
+def test_gumbel_max_samples_the_softmax():
+    """argmax_k (l_k + g_k) ~ Categorical(softmax(l)) (the Gumbel-max identity behind Alg. 1)."""
+    l = np.array([0.3, -1.2, 1.0, 0.1, -0.4])
+    n = 300_000
+    g = philox.gumbel(9, np.arange(n, dtype=np.int64), 0, 5)
+    k = np.argmax(l + g, axis=1)
+    p = np.exp(l) / np.exp(l).sum()
+    assert stats.chisquare(np.bincount(k, minlength=5), n * p).pvalue > 1e-4
+
+
+def test_init_normals_are_standard_normal():
+    z = philox.init_normals(2, np.arange(200_000, dtype=np.int64), 8).reshape(-1)
+    assert abs(z.mean()) < 5 / np.sqrt(z.size)
+    assert abs(z.var() - 1) < 5 * np.sqrt(2 / z.size)
+    assert stats.kstest(z[:200_000], "norm").pvalue > 1e-4
+    # the sine and cosine halves of one Box-Muller pair are uncorrelated
+    zz = philox.init_normals(2, np.arange(100_000, dtype=np.int64), 2)
+    assert abs(np.corrcoef(zz[:, 0], zz[:, 1])[0, 1]) < 5 / np.sqrt(zz.shape[0])
