@@ -1,0 +1,187 @@
+/*
+ * gsq.h -- C ABI of the GSQ layer-step library for MI355X (gfx950).
+ *
+ * The library optimises one linear layer (or a batch of independent layers,
+ * e.g. the routed experts of an MoE block) with Gumbel-Softmax Quantization
+ * (arXiv 2604.18556): find per-group scales s and per-coordinate grid codes q
+ * minimising the layer-output error of Eq. 1 on calibration data, under the
+ * b-bit scalar constraint W_hat = s * c[q] of Eq. 5 (§3.2), with groups of
+ * consecutive weights along each row (§4.1).  For a linear layer with
+ * calibration inputs X the objective of Eq. 1 is tr((W - W_hat) H (W - W_hat)^T)
+ * with H = X^T X, which is what the caller supplies.
+ *
+ * Every call only enqueues work on the caller's HIP stream and returns; the
+ * outputs are valid once the stream reaches that point.  Calls that must read
+ * a device result first (gsq_check, gsq_harden, gsq_pack, gsq_get_state)
+ * synchronise the stream themselves and say so.  Functions never throw and
+ * never abort; each returns a gsq_status and, on error, leaves a message for
+ * gsq_last_error() (thread-local).  Validation errors are returned before
+ * anything is enqueued or allocated.
+ *
+ * Pointers named "device" must point to device memory of the current HIP
+ * device (hipMalloc, torch CUDA tensors); "host" pointers to host memory.
+ * A handle must not be used from two threads at once; separate handles are
+ * independent.  All row-major arrays are dense (no strides).
+ */
+#ifndef GSQ_H
+#define GSQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct gsq_layer gsq_layer; /* opaque; owns every internal device buffer */
+
+typedef enum {
+  GSQ_OK = 0,
+  GSQ_EINVAL = -1,        /* invalid argument or configuration                         */
+  GSQ_ENOMEM = -2,        /* a device allocation failed                                */
+  GSQ_EHIP = -3,          /* a HIP runtime call failed; gsq_last_error() has its text  */
+  GSQ_ENONFINITE = -4,    /* a loss, gradient, updated parameter or fp16 scale was
+                             not finite (sticky until the handle is destroyed)         */
+  GSQ_EUNSUPPORTED = -5   /* valid request the library does not implement              */
+} gsq_status;
+
+enum { GSQ_LAYOUT_GROUP = 0, GSQ_LAYOUT_SUPERBLOCK = 1 };
+enum { GSQ_PREC_FP32 = 0, GSQ_PREC_BF16 = 1 };
+enum { GSQ_DT_FP32 = 0, GSQ_DT_BF16 = 1 };
+#define GSQ_MAX_LEVELS 8
+
+/* Layer configuration (read at gsq_layer_init; copied). */
+typedef struct {
+  int32_t  batch;          /* independent layers sharing the configuration (>= 1)           */
+  int32_t  out_features;   /* O (>= 1)                                                      */
+  int32_t  in_features;    /* I; multiple of group_size (GROUP) or of 256 (SUPERBLOCK)      */
+  int32_t  n_levels;       /* K, 2..8: grid cardinality |G_b| of Eq. 5                      */
+  float    levels[GSQ_MAX_LEVELS]; /* c_0 < ... < c_{K-1}, finite, not all zero              */
+  int32_t  group_size;     /* GROUP: 16, 32, 64, 128 or 256 consecutive inputs per scale;
+                              SUPERBLOCK: ignored (16-weight sub-blocks)                    */
+  int32_t  layout;         /* GSQ_LAYOUT_*: GROUP = one fp16 scale per group (Tab. 1 format);
+                              SUPERBLOCK = 256-weight records of 16 sub-blocks, each with a
+                              6-bit scale times one fp16 scale per record (K-quant style, §4.4) */
+  int32_t  precision;      /* GSQ_PREC_*: type of the residual R and of H in the contraction.
+                              BF16: bf16 operands, fp32 accumulation on the matrix cores,
+                              fp32 elementwise arithmetic with hardware log/exp.
+                              FP32: fp32 operands, fp64 accumulation, fp64 elementwise.     */
+  uint64_t seed;           /* key of the Philox4x32-10 noise generator                      */
+  float    alpha;          /* warm-start strength of Eq. 4 (the paper uses 6 for 2/3-bit)   */
+  float    sigma_init;     /* overall logit scale of Eq. 4                                  */
+  int32_t  init_noise;     /* 1: add N(0,1) noise to the initial logits (Eq. 4); 0: none    */
+} gsq_config;
+
+/* Scalars of one optimisation step (host values; the schedule lives with the caller). */
+typedef struct {
+  float   tau;             /* temperature of Alg. 1 (> 0)                                   */
+  float   kappa;           /* logit ("noise") scale of Alg. 1 (finite)                      */
+  float   lr_logits;       /* Adam step size of the logits (>= 0)                           */
+  float   lr_scales;       /* Adam step size of the scales; 0 freezes them (required for
+                              SUPERBLOCK, whose scales stay in their 6-bit grid)            */
+  float   beta1, beta2;    /* Adam moment decays, in [0, 1)                                 */
+  float   eps;             /* Adam denominator constant (> 0)                               */
+  int32_t gumbel_noise;    /* 1: sample g ~ Gumbel(0,1) (Alg. 1); 0: g = 0                  */
+  float   tau_next;        /* temperature of the NEXT call's step, or 0 if unknown.  When
+                              the next call passes exactly (tau_next, kappa_next) the sample
+                              of that step has already been drawn by this one, saving one
+                              pass over the logits.  Results are identical either way.      */
+  float   kappa_next;      /* logit scale of the next step (used when tau_next > 0)         */
+} gsq_step_params;
+
+/*
+ * Create a layer.  W: device, batch x O x I row-major, fp32 or bf16 (w_dtype).
+ * H: device fp32, batch x I x I row-major; only its symmetric part (H + H^T)/2
+ * matters and the library keeps that (in the precision's type).
+ * scales_init: device fp32 batch x O x (I/group_size), or NULL for
+ * round-to-nearest absmax scales s = max|W_group| / max_k |c_k| (1 for an all-zero
+ * group); must be NULL for SUPERBLOCK.  The logits start from the Gaussian prior
+ * around the round-to-nearest codes (App. A) plus Eq. 4's noise; moments are zero,
+ * the step counter t is 0.  W and H are copied: the caller may free them once the
+ * stream has passed this call.  On success *out receives the handle.
+ */
+gsq_status gsq_layer_init(const gsq_config* cfg, const void* W, int32_t w_dtype, const float* H,
+                          const float* scales_init, hipStream_t stream, gsq_layer** out);
+
+/*
+ * One optimisation step (Alg. 1 sample, Eq. 1 loss, gradient, Adam; the paper's
+ * Alg. 2 loop body generalised to K levels by §3.2): draws g for step t, forms
+ * the soft weight s * sum_k p_k c_k, the residual R, P = R H, the loss
+ * tr(R H R^T), the gradients of the logits and scales, applies Adam (bias
+ * correction at step t+1) and advances t.  loss_out: device fp32[batch]
+ * receiving the loss of this step's sample before the update, or NULL to skip
+ * computing it.
+ */
+gsq_status gsq_step(gsq_layer* h, const gsq_step_params* p, float* loss_out, hipStream_t stream);
+
+/*
+ * Harden (the final argmax of Alg. 2, K-way): codes q = argmax_k logits (ties to the
+ * lowest k) into `codes` (device u8, batch x O x I, or NULL); effective scales
+ * into `scales` (device fp32, batch x O x (I/group_size) -- GROUP: the fp16-rounded
+ * scales, SUPERBLOCK: d * sc per 16-weight sub-block; or NULL); the hard loss
+ * tr(R H R^T) with R = W - s c[q] into hard_loss_out (device fp32[batch], or NULL).
+ * Synchronises the stream; returns GSQ_ENONFINITE if a scale overflows fp16 or the
+ * sticky non-finite flag is set.
+ */
+gsq_status gsq_harden(gsq_layer* h, uint8_t* codes, float* scales, float* hard_loss_out,
+                      hipStream_t stream);
+
+/* Bytes gsq_pack writes for this configuration (0 if the configuration is invalid).
+ * GROUP: batch*O*I*b/8 code bytes (b = ceil(log2 K)) + 2*batch*O*(I/group_size) scale bytes;
+ * SUPERBLOCK: 110 bytes per 256 weights. */
+size_t gsq_packed_size(const gsq_config* cfg);
+
+/*
+ * Pack the hardened layer into `packed` (device, >= gsq_packed_size bytes).
+ * GROUP: one little-endian bitstream of b-bit codes (code = level index) over all
+ * coordinates in row-major order, then the fp16 scales row-major.  SUPERBLOCK: per
+ * 256 consecutive weights of a row, [fp16 d][16 x 6-bit sc, LSB first][256 x 3-bit
+ * codes, LSB first] = 110 bytes, records row-major.  Synchronises the stream.
+ */
+gsq_status gsq_pack(gsq_layer* h, void* packed, size_t packed_bytes, hipStream_t stream);
+
+/*
+ * Copy the optimiser state out (device pointers, any may be NULL):
+ * logits, m, v: fp32 batch x O x I x K; scales, m_s, v_s: fp32 batch x O x (I/gs)
+ * (gs = 16 for SUPERBLOCK); t: host int64.  Synchronises the stream.
+ */
+gsq_status gsq_get_state(gsq_layer* h, float* logits, float* m, float* v, float* scales,
+                         float* m_s, float* v_s, int64_t* t, hipStream_t stream);
+
+/* Overwrite the state (same layouts; NULL leaves that part unchanged; t >= 0). */
+gsq_status gsq_set_state(gsq_layer* h, const float* logits, const float* m, const float* v,
+                         const float* scales, const float* m_s, const float* v_s, int64_t t,
+                         hipStream_t stream);
+
+/*
+ * Intermediates of the most recent gsq_step (device pointers, either may be NULL):
+ * residual R = W - W_hat of that step's sample, batch x O x I, in the precision's
+ * type (fp32 or bf16); grad = dL/dW_hat = -2 R H, fp32 batch x O x I.
+ * GSQ_EINVAL if no step has run since init / set_state / harden.
+ */
+gsq_status gsq_get_intermediates(gsq_layer* h, void* residual, float* grad, hipStream_t stream);
+
+/*
+ * The Gumbel noise the step kernels draw (Alg. 1): g for the `count` coordinates
+ * starting at global index e0 (e = ((b*O)+o)*I + i) at step t, K values each,
+ * into g_out (device fp32, count x K).  Uses cfg's seed, n_levels and precision
+ * (FP32: -ln(-ln u) evaluated in fp64 and rounded; BF16: hardware log2).
+ */
+gsq_status gsq_gumbel(const gsq_config* cfg, int64_t e0, int64_t count, int64_t t, float* g_out,
+                      hipStream_t stream);
+
+/* Synchronise the stream and report the sticky non-finite flag (GSQ_OK or GSQ_ENONFINITE). */
+gsq_status gsq_check(gsq_layer* h, hipStream_t stream);
+
+/* Free every buffer of the handle (NULL-safe; synchronises the device). */
+gsq_status gsq_layer_destroy(gsq_layer* h);
+
+/* Message of the last error on this thread ("" if none). */
+const char* gsq_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GSQ_H */

@@ -218,7 +218,8 @@ def init_logits(q0, cfg, eps=None):
     """Eq. 4: l = sigma_init * (eps + alpha * l_prior); eps ~ N(0, I) or zero."""
     lp = prior_logits(q0, cfg)
     noise = 0.0 if eps is None else eps
-    return round_f32(cfg.sigma_init * (noise + cfg.alpha * lp)).astype(np.float32)
+    sigma, alpha = float(np.float32(cfg.sigma_init)), float(np.float32(cfg.alpha))
+    return round_f32(sigma * (noise + alpha * lp)).astype(np.float32)
 
 
 def coord_index(cfg, b, rows):
@@ -228,10 +229,19 @@ def coord_index(cfg, b, rows):
     return ((b * cfg.out_features + rows)[:, None] * cfg.in_features + i[None, :]).reshape(-1)
 
 
-def init_layer(cfg, W, scales_init=None):
-    """Initial state of ``gsq_layer_init``: scales, RTN codes, logits, zero moments."""
+def init_layer(cfg, W, scales_init=None, rows=None):
+    """Initial state of ``gsq_layer_init``: scales, RTN codes, logits, zero moments.
+
+    ``rows`` restricts the state to a subset of the rows of every layer (every
+    quantity of the initialisation is row-local); noise indices stay global.
+    """
     W = np.asarray(W, dtype=np.float64).reshape(cfg.batch, cfg.out_features, cfg.in_features)
     B, O, I, K = cfg.batch, cfg.out_features, cfg.in_features, cfg.K
+    rows = np.arange(O) if rows is None else np.asarray(rows)
+    W = W[:, rows]
+    if scales_init is not None:
+        scales_init = np.asarray(scales_init, np.float32).reshape(B, O, I // cfg.gs)[:, rows]
+    O = len(rows)
     sb_d = sb_sc = None
     if cfg.layout == "superblock":
         sb_d, sb_sc, scales = superblock_scales(W, cfg)
@@ -244,7 +254,7 @@ def init_layer(cfg, W, scales_init=None):
     for b in range(B):
         eps = None
         if cfg.init_noise:
-            e = coord_index(cfg, b, np.arange(O))
+            e = coord_index(cfg, b, rows)
             eps = philox.init_normals(cfg.seed, e, K).reshape(O, I, K)
         logits[b] = init_logits(q0[b], cfg, eps)
     z = np.zeros_like(logits)
@@ -331,7 +341,8 @@ def step(cfg, W, Hs, st, prm, rows=None, want=False):
     the one of this step's sample, before the update.
 
     ``rows`` restricts the step to a subset of the rows of every layer (rows
-    are independent given H); noise indices stay the global ones.
+    are independent given H); ``st`` then holds just those rows and noise
+    indices stay the global ones.
     ``want`` returns the intermediates (g, p, v, R, G, dlogits, dscales).
     """
     B, O, I, K = cfg.batch, cfg.out_features, cfg.in_features, cfg.K
@@ -349,8 +360,8 @@ def step(cfg, W, Hs, st, prm, rows=None, want=False):
             g = philox.gumbel(cfg.seed, e, st.t, K).reshape(len(rows), I, K)
         else:
             g = np.zeros((len(rows), I, K))
-        lg = st.logits[b, rows]
-        sc = st.scales[b, rows]
+        lg = st.logits[b]
+        sc = st.scales[b]
         s_coord = expand_scales(sc, cfg.gs)
         p, v, R = forward(cfg, W[b], lg, s_coord, g, prm.tau, prm.kappa)
         P, L = contract(cfg, R, Hs[b])
@@ -358,13 +369,13 @@ def step(cfg, W, Hs, st, prm, rows=None, want=False):
         dlog, dsc = backward(cfg, G[None], s_coord[None], p[None], v[None], prm.tau, prm.kappa)
         dlog, dsc = dlog[0], dsc[0]
         losses[b] = L
-        th, m1, v1 = adam(lg, st.m[b, rows], st.v[b, rows], dlog, prm.lr_logits,
-                          prm.beta1, prm.beta2, prm.eps, n)
-        new.logits[b, rows], new.m[b, rows], new.v[b, rows] = th, m1, v1
+        th, m1, v1 = adam(lg, st.m[b], st.v[b], dlog, prm.lr_logits, prm.beta1, prm.beta2,
+                          prm.eps, n)
+        new.logits[b], new.m[b], new.v[b] = th, m1, v1
         if prm.lr_scales > 0:
-            ts, ms, vs = adam(sc, st.m_s[b, rows], st.v_s[b, rows], dsc, prm.lr_scales,
-                              prm.beta1, prm.beta2, prm.eps, n)
-            new.scales[b, rows], new.m_s[b, rows], new.v_s[b, rows] = ts, ms, vs
+            ts, ms, vs = adam(sc, st.m_s[b], st.v_s[b], dsc, prm.lr_scales, prm.beta1, prm.beta2,
+                              prm.eps, n)
+            new.scales[b], new.m_s[b], new.v_s[b] = ts, ms, vs
         if want:
             for k, val in zip(inter, (g, p, v, R, G, dlog, dsc)):
                 inter[k].append(val)

@@ -1,0 +1,225 @@
+// The dense contraction of the GSQ step: P = R H for every row of the residual R = W - W_hat,
+// the gradient G = dL/dW_hat = -2 P (H symmetric) and, on request, per-tile partial sums of
+// the loss tr(R H R^T) = sum(R * P) (Eq. 1 for a linear layer, H = X^T X).
+//
+// BF16 precision: R and H in bf16, products accumulated in fp32 on the matrix cores
+// (v_mfma 32x32x16 bf16).  Because H is symmetric, column i of H is row i, so both operands
+// are read along their contiguous dimension.
+// FP32 precision: fp32 operands, fp64 accumulation on the vector units.
+#include <hip/hip_runtime.h>
+
+#include "gsq_device.hpp"
+#include "gsq_internal.h"
+
+namespace gsq {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int BM = kTileM, BN = kTileN, BK = 32;
+constexpr int LDS_STRIDE = BK + 8;   // bf16 per LDS row; 16 bytes of padding against bank conflicts
+
+__device__ __forceinline__ void block_sum_to(double x, double* out) {
+  __shared__ double red[256];
+  red[threadIdx.x] = x;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *out = red[0];
+}
+
+// One 128 x 128 tile of G per workgroup; four wavefronts each own 64 x 64 as 2 x 2 MFMA tiles.
+__global__ __launch_bounds__(256) void k_contract_bf16(const uint16_t* __restrict__ R,
+                                                       const uint16_t* __restrict__ H,
+                                                       float* __restrict__ G,
+                                                       double* __restrict__ partials, int64_t Opad,
+                                                       int64_t Ipad, int want_loss) {
+  __shared__ __attribute__((aligned(16))) uint16_t As[BM * LDS_STRIDE];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[BN * LDS_STRIDE];
+  const int64_t b = blockIdx.z;
+  const int64_t m0 = (int64_t)blockIdx.y * BM, n0 = (int64_t)blockIdx.x * BN;
+  const uint16_t* A = R + b * Opad * Ipad + m0 * Ipad;
+  const uint16_t* Bt = H + b * Ipad * Ipad + n0 * Ipad;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  // 128 rows x 32 bf16 per operand tile = 512 chunks of 16 bytes, two per thread
+  uint4 ra[2], rb[2];
+  auto gload = [&](int64_t k0) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int c = tid + 256 * i, row = c >> 2, col = (c & 3) * 8;
+      ra[i] = *reinterpret_cast<const uint4*>(A + row * Ipad + k0 + col);
+      rb[i] = *reinterpret_cast<const uint4*>(Bt + row * Ipad + k0 + col);
+    }
+  };
+  auto lstore = [&]() {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int c = tid + 256 * i, row = c >> 2, col = (c & 3) * 8;
+      *reinterpret_cast<uint4*>(As + row * LDS_STRIDE + col) = ra[i];
+      *reinterpret_cast<uint4*>(Bs + row * LDS_STRIDE + col) = rb[i];
+    }
+  };
+
+  const int64_t nk = Ipad / BK;
+  gload(0);
+  lstore();
+  __syncthreads();
+  for (int64_t kt = 0; kt < nk; ++kt) {
+    if (kt + 1 < nk) gload((kt + 1) * BK);
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      bf16x8 af[2], bv[2];
+      const int col = ks * 16 + (lane >> 5) * 8;
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        af[i] = *reinterpret_cast<const bf16x8*>(As + (wm * 64 + i * 32 + (lane & 31)) * LDS_STRIDE + col);
+        bv[i] = *reinterpret_cast<const bf16x8*>(Bs + (wn * 64 + i * 32 + (lane & 31)) * LDS_STRIDE + col);
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bv[j], acc[i][j], 0, 0, 0);
+    }
+    __syncthreads();
+    if (kt + 1 < nk) {
+      lstore();
+      __syncthreads();
+    }
+  }
+
+  // 32 x 32 accumulator layout: lane l, register r -> row 8*(r/4) + 4*(l/32) + r%4, column l%32
+  float* Gb = G + b * Opad * Ipad;
+  const uint16_t* Rb = R + b * Opad * Ipad;
+  double lsum = 0.0;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t row = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        const int64_t col = n0 + wn * 64 + j * 32 + (lane & 31);
+        const float p = acc[i][j][r];
+        Gb[row * Ipad + col] = -2.f * p;
+        if (want_loss) lsum += (double)bf16_to_f32(Rb[row * Ipad + col]) * (double)p;
+      }
+  if (want_loss)
+    block_sum_to(lsum, partials + (b * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x);
+}
+
+// FP32 precision: 64 x 64 tile per workgroup, 4 x 4 outputs per thread, fp64 accumulation.
+constexpr int TM = 64, TN = 64, TK = 16;
+
+__global__ __launch_bounds__(256) void k_contract_f32(const float* __restrict__ R,
+                                                      const float* __restrict__ H,
+                                                      float* __restrict__ G,
+                                                      double* __restrict__ partials, int64_t Opad,
+                                                      int64_t Ipad, int want_loss) {
+  __shared__ float As[TK][TM + 1];
+  __shared__ float Bs[TK][TN + 1];
+  const int64_t b = blockIdx.z;
+  const int64_t m0 = (int64_t)blockIdx.y * TM, n0 = (int64_t)blockIdx.x * TN;
+  const float* A = R + b * Opad * Ipad + m0 * Ipad;
+  const float* Bt = H + b * Ipad * Ipad + n0 * Ipad;
+  const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
+  double acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
+  for (int64_t k0 = 0; k0 < Ipad; k0 += TK) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = tid + 256 * i, row = c >> 4, k = c & 15;
+      As[k][row] = A[row * Ipad + k0 + k];
+      Bs[k][row] = Bt[row * Ipad + k0 + k];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < TK; ++k) {
+      double av[4], bv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) { av[i] = As[k][ty * 4 + i]; bv[i] = Bs[k][tx * 4 + i]; }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fma(av[i], bv[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+  double lsum = 0.0;
+  float* Gb = G + b * Opad * Ipad;
+  const float* Rb = R + b * Opad * Ipad;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t row = m0 + ty * 4 + i, col = n0 + tx * 4 + j;
+      Gb[row * Ipad + col] = (float)(-2.0 * acc[i][j]);
+      if (want_loss) lsum += (double)Rb[row * Ipad + col] * acc[i][j];
+    }
+  if (want_loss)
+    block_sum_to(lsum, partials + (b * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x);
+}
+
+// Loss of layer b = sum of its tile partials, in a fixed order.
+__global__ void k_reduce_loss(const double* partials, int64_t per_batch, float* loss_out, int* flag) {
+  const int64_t b = blockIdx.x;
+  double s = 0.0;
+  for (int64_t i = threadIdx.x; i < per_batch; i += 256) s += partials[b * per_batch + i];
+  __shared__ double red[256];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const float L = (float)red[0];
+    loss_out[b] = L;
+    if (!__builtin_isfinite(L)) *flag = 1;
+  }
+}
+
+}  // namespace
+
+int64_t contract_tiles_per_batch(const Layer& L) {
+  return L.bf16 ? (L.Opad / BM) * (L.Ipad / BN) : (L.Opad / TM) * (L.Ipad / TN);
+}
+
+hipError_t launch_contract(const Layer& L, const void* R, bool want_loss, hipStream_t s) {
+  if (L.bf16) {
+    dim3 grid((unsigned)(L.Ipad / BN), (unsigned)(L.Opad / BM), (unsigned)L.B);
+    hipLaunchKernelGGL(k_contract_bf16, grid, dim3(256), 0, s, static_cast<const uint16_t*>(R),
+                       static_cast<const uint16_t*>(L.H), L.G, L.partials, L.Opad, L.Ipad,
+                       want_loss ? 1 : 0);
+  } else {
+    dim3 grid((unsigned)(L.Ipad / TN), (unsigned)(L.Opad / TM), (unsigned)L.B);
+    hipLaunchKernelGGL(k_contract_f32, grid, dim3(256), 0, s, static_cast<const float*>(R),
+                       static_cast<const float*>(L.H), L.G, L.partials, L.Opad, L.Ipad,
+                       want_loss ? 1 : 0);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_loss(const Layer& L, float* loss_out, hipStream_t s) {
+  hipLaunchKernelGGL(k_reduce_loss, dim3((unsigned)L.B), dim3(256), 0, s, L.partials,
+                     contract_tiles_per_batch(L), loss_out, L.flag);
+  return hipGetLastError();
+}
+
+}  // namespace gsq

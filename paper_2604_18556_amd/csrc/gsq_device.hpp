@@ -1,0 +1,80 @@
+// Device helpers of the GSQ kernels: Philox4x32-10, the noise transforms, bf16 rounding.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gsq {
+
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds, each multiplying words
+// 0 and 2 by the round multipliers and mixing the 64-bit products' halves with the other
+// words and the round key; the key advances by the two Weyl constants between rounds.
+struct U4 { uint32_t x, y, z, w; };
+
+__device__ __forceinline__ U4 philox10(U4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c.x;
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * c.z;
+    c = U4{(uint32_t)(p1 >> 32) ^ c.y ^ k0, (uint32_t)p1, (uint32_t)(p0 >> 32) ^ c.w ^ k1,
+           (uint32_t)p0};
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  return c;
+}
+
+// Counter of coordinate e, step t, stream (0 = step noise, 1 = initial logit noise), block j
+// of four levels: (e mod 2^32, e >> 32, t, stream*256 + j); key = seed.
+__device__ __forceinline__ U4 noise_words(uint64_t seed, uint64_t e, uint32_t t, uint32_t stream,
+                                          uint32_t j) {
+  return philox10(U4{(uint32_t)e, (uint32_t)(e >> 32), t, stream * 256u + j}, (uint32_t)seed,
+                  (uint32_t)(seed >> 32));
+}
+
+// u = (top 23 bits + 1/2) * 2^-23, exact in fp32, in [2^-24, 1 - 2^-24].
+__device__ __forceinline__ float uniform01(uint32_t x) {
+  return ((float)(x >> 9) + 0.5f) * 0x1p-23f;
+}
+
+// Gumbel(0,1) sample -ln(-ln u): evaluated in fp64 and rounded once to fp32.
+__device__ __forceinline__ float gumbel_exact(uint32_t x) {
+  const double u = (double)uniform01(x);
+  return (float)(-log(-log(u)));
+}
+
+// Gumbel(0,1) sample with the hardware base-2 logarithm:
+// -ln(-ln u) = -ln2 * log2(-ln2 * log2 u).
+__device__ __forceinline__ float gumbel_fast(uint32_t x) {
+  constexpr float kLn2 = 0.69314718055994531f;
+  const float u = uniform01(x);
+  const float nl = __builtin_amdgcn_logf(u) * -kLn2;   // -ln u > 0
+  return __builtin_amdgcn_logf(nl) * -kLn2;
+}
+
+template <bool kExact>
+__device__ __forceinline__ float gumbel(uint32_t x) {
+  if constexpr (kExact) return gumbel_exact(x); else return gumbel_fast(x);
+}
+
+// The K Gumbel values of coordinate e at step t.
+template <int K, bool kExact>
+__device__ __forceinline__ void draw_gumbel(float (&g)[K], uint64_t seed, uint64_t e, uint32_t t) {
+#pragma unroll
+  for (int j = 0; j < (K + 3) / 4; ++j) {
+    const U4 w = noise_words(seed, e, t, 0u, (uint32_t)j);
+    const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (4 * j + r < K) g[4 * j + r] = gumbel<kExact>(ws[r]);
+  }
+}
+
+// float -> bf16 bits, round to nearest even (finite inputs).
+__device__ __forceinline__ uint16_t bf16_rne(float f) {
+  uint32_t b = __float_as_uint(f);
+  b += 0x7FFFu + ((b >> 16) & 1u);
+  return (uint16_t)(b >> 16);
+}
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+}  // namespace gsq

@@ -1,0 +1,681 @@
+// Elementwise kernels of the GSQ layer step on gfx950: initialisation (Eq. 4, App. A),
+// the Gumbel-Softmax sample of Alg. 1 and its residual, the fused gradient + Adam pass,
+// hardening (argmax of Alg. 2) and bit-packing.
+//
+// Data layout in HBM: logits and both Adam moments are K planes of N = B*O*I fp32 values
+// (plane k holds level k of every coordinate, row-major), so every plane streams with
+// 16-byte loads across a wavefront.  A wavefront owns 256 consecutive columns of one row;
+// lane l owns columns 4l..4l+3.  Scale groups (16..256 columns) therefore lie inside one
+// wavefront and their gradient is reduced with lane shuffles in a fixed order.
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+
+#include <type_traits>
+
+#include "gsq_device.hpp"
+#include "gsq_internal.h"
+
+namespace gsq {
+namespace {
+
+constexpr int kBlock = 256;   // 4 wavefronts
+constexpr int kCols = 256;    // columns per wavefront
+
+template <bool kF64>
+using Real = typename std::conditional<kF64, double, float>::type;
+
+__device__ __forceinline__ float f4get(const float4& v, int q) {
+  return q == 0 ? v.x : q == 1 ? v.y : q == 2 ? v.z : v.w;
+}
+__device__ __forceinline__ void f4set(float4& v, int q, float x) {
+  if (q == 0) v.x = x; else if (q == 1) v.y = x; else if (q == 2) v.z = x; else v.w = x;
+}
+
+__device__ __forceinline__ void load_w4(const void* W, int w_bf16, int64_t e, float (&w)[4]) {
+  if (w_bf16) {
+    const uint2 u = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(W) + e);
+    w[0] = __uint_as_float(u.x << 16);
+    w[1] = __uint_as_float(u.x & 0xFFFF0000u);
+    w[2] = __uint_as_float(u.y << 16);
+    w[3] = __uint_as_float(u.y & 0xFFFF0000u);
+  } else {
+    const float4 v = *reinterpret_cast<const float4*>(static_cast<const float*>(W) + e);
+    w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
+  }
+}
+
+// R is stored in the contraction's padded layout: row (b, o) at (b*Opad + o)*Ipad.
+__device__ __forceinline__ int64_t padded_index(const ElemArgs& a, int64_t row, int64_t col) {
+  const int64_t b = row / a.O;
+  return (b * a.Opad + (row - b * a.O)) * a.Ipad + col;
+}
+
+template <bool kF64>
+__device__ __forceinline__ void store_r4(void* R, int64_t idx, const float (&r)[4]) {
+  if constexpr (kF64) {
+    *reinterpret_cast<float4*>(static_cast<float*>(R) + idx) = make_float4(r[0], r[1], r[2], r[3]);
+  } else {
+    uint2 u;
+    u.x = (uint32_t)bf16_rne(r[0]) | ((uint32_t)bf16_rne(r[1]) << 16);
+    u.y = (uint32_t)bf16_rne(r[2]) | ((uint32_t)bf16_rne(r[3]) << 16);
+    *reinterpret_cast<uint2*>(static_cast<uint16_t*>(R) + idx) = u;
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ T exp_t(T x) {
+  if constexpr (std::is_same<T, double>::value) return exp(x); else return __expf(x);
+}
+
+// One coordinate's relaxed sample (Alg. 1): p = softmax((kappa l + g) / tau), with the
+// largest perturbed logit r subtracted first.  vp = sum_k p_k (c_k - c_r), so that the soft
+// level v = c_r + vp and c_k - v = (c_k - c_r) - vp keep full relative accuracy when one
+// level holds almost all the mass.
+template <int K, bool kF64>
+__device__ __forceinline__ void soft_sample(const float (&l)[K], const float (&c)[8], uint64_t seed,
+                                            uint64_t e, uint32_t t, bool noise, float kappa,
+                                            Real<kF64> inv_tau, Real<kF64> (&p)[K],
+                                            Real<kF64>& vp, Real<kF64>& cr) {
+  using T = Real<kF64>;
+  float g[K];
+  if (noise) {
+    draw_gumbel<K, kF64>(g, seed, e, t);
+  } else {
+#pragma unroll
+    for (int k = 0; k < K; ++k) g[k] = 0.f;
+  }
+  T b[K];
+#pragma unroll
+  for (int k = 0; k < K; ++k) b[k] = (T)kappa * (T)l[k] + (T)g[k];
+  T bmax = b[0];
+  cr = (T)c[0];
+#pragma unroll
+  for (int k = 1; k < K; ++k) {
+    if (b[k] > bmax) { bmax = b[k]; cr = (T)c[k]; }
+  }
+  T z = 0;
+#pragma unroll
+  for (int k = 0; k < K; ++k) { p[k] = exp_t<T>((b[k] - bmax) * inv_tau); z += p[k]; }
+  const T rz = T(1) / z;
+  vp = 0;
+#pragma unroll
+  for (int k = 0; k < K; ++k) { p[k] *= rz; vp += p[k] * ((T)c[k] - cr); }
+}
+
+// ------------------------------------------------------------------ forward: R = W - s * v
+template <int K, bool kF64>
+__global__ __launch_bounds__(kBlock) void k_forward(ElemArgs a) {
+  using T = Real<kF64>;
+  const int lane = threadIdx.x & 63;
+  const int64_t col0 = (int64_t)blockIdx.x * kCols + lane * 4;
+  const T inv_tau = kF64 ? (T)a.inv_tau_d : (T)a.inv_tau;
+  const int64_t gpr = a.I / a.gs;
+  for (int64_t row = (int64_t)blockIdx.y * 4 + (threadIdx.x >> 6); row < a.rows;
+       row += (int64_t)gridDim.y * 4) {
+    if (col0 >= a.I) continue;
+    const int64_t e0 = row * a.I + col0;
+    const T s = (T)a.S[row * gpr + col0 / a.gs];
+    float w[4];
+    load_w4(a.W, a.w_bf16, e0, w);
+    float4 lv[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) lv[k] = *reinterpret_cast<const float4*>(a.L + k * a.N + e0);
+    float r[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      float l[K];
+#pragma unroll
+      for (int k = 0; k < K; ++k) l[k] = f4get(lv[k], q);
+      T p[K], vp, cr;
+      soft_sample<K, kF64>(l, a.c, a.seed, (uint64_t)(e0 + q), a.t, a.noise != 0, a.kappa, inv_tau,
+                           p, vp, cr);
+      r[q] = (float)((T)w[q] - s * (cr + vp));
+    }
+    store_r4<kF64>(a.Rout, padded_index(a, row, col0), r);
+  }
+}
+
+// ------------------------------------------------------------------ gradient + Adam (+ next sample)
+// dL/dl_k = (kappa / tau) G s p_k (c_k - v); dL/ds = sum over the group of G v.  Adam with
+// bias correction at step n = t + 1.  With a.fuse, the sample of step t + 1 is drawn from
+// the updated logits and scale and its residual written to a.Rout.
+template <int K, bool kF64, bool kScales>
+__global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
+  using T = Real<kF64>;
+  const int lane = threadIdx.x & 63;
+  const int64_t col0 = (int64_t)blockIdx.x * kCols + lane * 4;
+  const bool active = col0 < a.I;
+  const T inv_tau = kF64 ? (T)a.inv_tau_d : (T)a.inv_tau;
+  const T kt = (T)a.kappa * inv_tau;
+  const T b1 = (T)a.b1, b2 = (T)a.b2, omb1 = T(1) - (T)a.b1, omb2 = T(1) - (T)a.b2;
+  const T eps = (T)a.eps;
+  const T step_l = kF64 ? (T)a.step_l_d : (T)a.step_l;
+  const T rbc2 = kF64 ? (T)a.rbc2_d : (T)a.rbc2;
+  const int lpg = a.gs / 4;   // lanes per scale group
+  const int64_t gpr = a.I / a.gs;
+  bool bad = false;
+  for (int64_t row = (int64_t)blockIdx.y * 4 + (threadIdx.x >> 6); row < a.rows;
+       row += (int64_t)gridDim.y * 4) {
+    const int64_t e0 = row * a.I + (active ? col0 : 0);
+    const int64_t sidx = row * gpr + (active ? col0 / a.gs : 0);
+    const float s32 = a.S[sidx];
+    const T s = (T)s32;
+    float4 gv = make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 lv[K], mv[K], vv[K];
+    if (active) {
+      gv = *reinterpret_cast<const float4*>(a.G + padded_index(a, row, col0));
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        lv[k] = *reinterpret_cast<const float4*>(a.L + k * a.N + e0);
+        mv[k] = *reinterpret_cast<const float4*>(a.M + k * a.N + e0);
+        vv[k] = *reinterpret_cast<const float4*>(a.V + k * a.N + e0);
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < K; ++k) lv[k] = mv[k] = vv[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    T ds_part = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      float l[K];
+#pragma unroll
+      for (int k = 0; k < K; ++k) l[k] = f4get(lv[k], q);
+      T p[K], vp, cr;
+      soft_sample<K, kF64>(l, a.c, a.seed, (uint64_t)(e0 + q), a.t, a.noise != 0, a.kappa, inv_tau,
+                           p, vp, cr);
+      const T gq = (T)f4get(gv, q);
+      ds_part += gq * (cr + vp);
+      const T coef = kt * (gq * s);
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        const T d = coef * p[k] * (((T)a.c[k] - cr) - vp);
+        const T m1 = b1 * (T)f4get(mv[k], q) + omb1 * d;
+        const T v1 = b2 * (T)f4get(vv[k], q) + omb2 * d * d;
+        const T l1 = (T)l[k] - step_l * m1 / (sqrt(v1) * rbc2 + eps);
+        f4set(mv[k], q, (float)m1);
+        f4set(vv[k], q, (float)v1);
+        f4set(lv[k], q, (float)l1);
+      }
+    }
+    if (active) {
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        bad |= !(__builtin_isfinite(lv[k].x) && __builtin_isfinite(lv[k].y) &&
+                 __builtin_isfinite(lv[k].z) && __builtin_isfinite(lv[k].w) &&
+                 __builtin_isfinite(vv[k].x) && __builtin_isfinite(vv[k].y) &&
+                 __builtin_isfinite(vv[k].z) && __builtin_isfinite(vv[k].w));
+        *reinterpret_cast<float4*>(a.L + k * a.N + e0) = lv[k];
+        *reinterpret_cast<float4*>(a.M + k * a.N + e0) = mv[k];
+        *reinterpret_cast<float4*>(a.V + k * a.N + e0) = vv[k];
+      }
+    }
+    float s_new = s32;
+    if constexpr (kScales) {
+      // fixed-order butterfly over the lanes of the group; the group's first lane owns the sum
+      for (int off = 1; off < lpg; off <<= 1) ds_part += __shfl_xor(ds_part, off, 64);
+      const bool leader = active && (lane & (lpg - 1)) == 0;
+      if (leader) {
+        const T step_s = kF64 ? (T)a.step_s_d : (T)a.step_s;
+        const T m1 = b1 * (T)a.MS[sidx] + omb1 * ds_part;
+        const T v1 = b2 * (T)a.VS[sidx] + omb2 * ds_part * ds_part;
+        s_new = (float)(s - step_s * m1 / (sqrt(v1) * rbc2 + eps));
+        bad |= !(__builtin_isfinite(s_new) && __builtin_isfinite((float)v1));
+        a.MS[sidx] = (float)m1;
+        a.VS[sidx] = (float)v1;
+        a.S[sidx] = s_new;
+      }
+      s_new = __shfl(s_new, lane & ~(lpg - 1), 64);
+    }
+    if (a.fuse && active) {
+      const T inv_tau_n = kF64 ? (T)a.inv_tau_n_d : (T)a.inv_tau_n;
+      float w[4];
+      load_w4(a.W, a.w_bf16, e0, w);
+      float r[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float l[K];
+#pragma unroll
+        for (int k = 0; k < K; ++k) l[k] = f4get(lv[k], q);
+        T p[K], vp, cr;
+        soft_sample<K, kF64>(l, a.c, a.seed, (uint64_t)(e0 + q), a.t_next, a.noise != 0, a.kappa_n,
+                             inv_tau_n, p, vp, cr);
+        r[q] = (float)((T)w[q] - (T)s_new * (cr + vp));
+      }
+      store_r4<kF64>(a.Rout, padded_index(a, row, col0), r);
+    }
+  }
+  if (bad) *a.flag = 1;
+}
+
+// ------------------------------------------------------------------ initialisation
+__global__ void k_symmetrize(const float* __restrict__ Hin, void* Hout, int64_t I, int64_t Ipad,
+                             int bf16) {
+  __shared__ float tile[32][33];
+  const int64_t b = blockIdx.z;
+  const int64_t i0 = (int64_t)blockIdx.y * 32, j0 = (int64_t)blockIdx.x * 32;
+  const float* H = Hin + b * I * I;
+  for (int r = threadIdx.y; r < 32; r += 8) {
+    const int64_t j = j0 + r, i = i0 + threadIdx.x;
+    tile[r][threadIdx.x] = (j < I && i < I) ? H[j * I + i] : 0.f;
+  }
+  __syncthreads();
+  for (int r = threadIdx.y; r < 32; r += 8) {
+    const int64_t i = i0 + r, j = j0 + threadIdx.x;
+    const float x = (i < I && j < I) ? H[i * I + j] : 0.f;
+    const float sym = (x + tile[threadIdx.x][r]) * 0.5f;
+    const int64_t o = b * Ipad * Ipad + i * Ipad + j;
+    if (bf16) static_cast<uint16_t*>(Hout)[o] = bf16_rne(sym);
+    else static_cast<float*>(Hout)[o] = sym;
+  }
+}
+
+__device__ __forceinline__ float load_w1(const void* W, int w_bf16, int64_t e) {
+  return w_bf16 ? bf16_to_f32(static_cast<const uint16_t*>(W)[e]) : static_cast<const float*>(W)[e];
+}
+
+// s = max|W_group| / max|c| (IEEE division), 1 for an all-zero group.
+__global__ void k_init_scales_group(const void* W, int w_bf16, float* S, int64_t ngroups, int gs,
+                                    float cmax) {
+  for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < ngroups;
+       g += (int64_t)gridDim.x * blockDim.x) {
+    float amax = 0.f;
+    for (int i = 0; i < gs; ++i) amax = fmaxf(amax, fabsf(load_w1(W, w_bf16, g * gs + i)));
+    const float s = __fdiv_rn(amax, cmax);
+    S[g] = s == 0.f ? 1.f : s;
+  }
+}
+
+// 256-weight super-block: d = fp16(max_j s_j / 63), sc_j = clamp(rint(s_j / d), 0, 63),
+// effective scale d * sc_j per 16-weight sub-block.
+__global__ void k_init_scales_superblock(const void* W, int w_bf16, float* S, uint16_t* D,
+                                         uint8_t* SC, int64_t nblocks, float cmax) {
+  for (int64_t sb = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; sb < nblocks;
+       sb += (int64_t)gridDim.x * blockDim.x) {
+    float raw[16];
+    float mx = 0.f;
+    for (int j = 0; j < 16; ++j) {
+      float amax = 0.f;
+      for (int i = 0; i < 16; ++i) amax = fmaxf(amax, fabsf(load_w1(W, w_bf16, sb * 256 + j * 16 + i)));
+      raw[j] = __fdiv_rn(amax, cmax);
+      mx = fmaxf(mx, raw[j]);
+    }
+    const __half dh = __float2half_rn(__fdiv_rn(mx, 63.f));
+    const float d = __half2float(dh);
+    D[sb] = __half_as_ushort(dh);
+    for (int j = 0; j < 16; ++j) {
+      const float q = d > 0.f ? __fdiv_rn(raw[j], d) : 0.f;
+      const float scq = fminf(fmaxf(rintf(q), 0.f), 63.f);
+      SC[sb * 16 + j] = (uint8_t)scq;
+      S[sb * 16 + j] = d * scq;
+    }
+  }
+}
+
+struct InitConsts {
+  float c[8];
+  double mids[8];   // (c_k + c_{k+1}) / 2, exact in fp64
+  int K;
+  float alpha, sigma;
+  int noise;
+  uint64_t seed;
+};
+
+// Round-to-nearest code (fp32 ratio, ties to the lower level), then the Gaussian prior of
+// App. A around it, mean-subtracted, plus Eq. 4's N(0,1) noise (Box-Muller on Philox stream 1):
+// l = sigma_init * (eps + alpha * prior).  fp64 arithmetic, fp32 storage.
+__global__ void k_init_logits(const void* W, int w_bf16, const float* S, float* L, int64_t N,
+                              int gs, InitConsts ic) {
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < N;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    const float w = load_w1(W, w_bf16, e);
+    const float s = S[e / gs];
+    const float u = s != 0.f ? __fdiv_rn(w, s) : 0.f;
+    int q = 0;
+    for (int k = 0; k + 1 < ic.K; ++k) q += ((double)u > ic.mids[k]) ? 1 : 0;
+    double cq = 0.0;
+    for (int k = 0; k < ic.K; ++k) if (k == q) cq = (double)ic.c[k];
+    double mu[8], mean = 0.0;
+    for (int k = 0; k < ic.K; ++k) {
+      const double dlt = (double)ic.c[k] - cq;
+      mu[k] = -0.5 * dlt * dlt;
+      mean += mu[k];
+    }
+    mean /= (double)ic.K;
+    float eps[8];
+    for (int k = 0; k < 8; ++k) eps[k] = 0.f;
+    if (ic.noise) {
+      for (int j = 0; j < (ic.K + 3) / 4; ++j) {
+        const U4 x = noise_words(ic.seed, (uint64_t)e, 0u, 1u, (uint32_t)j);
+        const double u0 = uniform01(x.x), u1 = uniform01(x.y), u2 = uniform01(x.z),
+                     u3 = uniform01(x.w);
+        const double r0 = sqrt(-2.0 * log(u0)), a0 = 2.0 * M_PI * u1;
+        const double r1 = sqrt(-2.0 * log(u2)), a1 = 2.0 * M_PI * u3;
+        eps[(4 * j + 0) & 7] = (float)(r0 * cos(a0));
+        eps[(4 * j + 1) & 7] = (float)(r0 * sin(a0));
+        eps[(4 * j + 2) & 7] = (float)(r1 * cos(a1));
+        eps[(4 * j + 3) & 7] = (float)(r1 * sin(a1));
+      }
+    }
+    for (int k = 0; k < ic.K; ++k)
+      L[k * N + e] = (float)((double)ic.sigma * ((double)eps[k] + (double)ic.alpha * (mu[k] - mean)));
+  }
+}
+
+// ------------------------------------------------------------------ hardening and packing
+// Codes q = argmax_k l_k (ties to the lowest k); optionally the hard residual R = W - s c[q]
+// (s rounded to fp16 in the group layout) written in the contraction's padded layout,
+// fp32 when r_f32 != 0, bf16 otherwise.
+__global__ void k_harden(ElemArgs a, int K, int superblock, int r_f32, uint8_t* codes, void* Rh) {
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < a.N;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    float best = a.L[e];
+    int q = 0;
+    for (int k = 1; k < K; ++k) {
+      const float x = a.L[k * a.N + e];
+      if (x > best) { best = x; q = k; }
+    }
+    if (codes) codes[e] = (uint8_t)q;
+    if (Rh) {
+      float s = a.S[e / a.gs];
+      if (!superblock) s = __half2float(__float2half_rn(s));
+      float cq = a.c[0];
+      for (int k = 1; k < K; ++k) if (k == q) cq = a.c[k];
+      const float r = load_w1(a.W, a.w_bf16, e) - s * cq;
+      const int64_t row = e / a.I;
+      const int64_t idx = padded_index(a, row, e - row * a.I);
+      if (r_f32) static_cast<float*>(Rh)[idx] = r;
+      else static_cast<uint16_t*>(Rh)[idx] = bf16_rne(r);
+    }
+  }
+}
+
+// Effective scales: fp16-rounded group scales (flag if one overflows), or the super-block
+// scales d * sc unchanged.
+__global__ void k_eff_scales(const float* S, float* out, int64_t n, int superblock, int* flag) {
+  for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < n;
+       g += (int64_t)gridDim.x * blockDim.x) {
+    float s = S[g];
+    if (!superblock) s = __half2float(__float2half_rn(s));
+    if (!__builtin_isfinite(s)) *flag = 1;
+    if (out) out[g] = s;
+  }
+}
+
+// Plain layout, code section: eight consecutive codes -> b bytes of the LSB-first bitstream.
+__global__ void k_pack_codes(const uint8_t* codes, uint8_t* out, int64_t n8, int b) {
+  for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n8;
+       j += (int64_t)gridDim.x * blockDim.x) {
+    const uint2 c8 = *reinterpret_cast<const uint2*>(codes + 8 * j);
+    uint32_t word = 0;
+    for (int q = 0; q < 8; ++q) {
+      const uint32_t code = ((q < 4 ? c8.x : c8.y) >> (8 * (q & 3))) & 0xFFu;
+      word |= code << (b * q);
+    }
+    for (int by = 0; by < b; ++by) out[j * b + by] = (uint8_t)(word >> (8 * by));
+  }
+}
+
+// Plain layout, scale section: fp16 scales, little endian.
+__global__ void k_pack_scales(const float* S, uint8_t* out, int64_t n, int* flag) {
+  for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < n;
+       g += (int64_t)gridDim.x * blockDim.x) {
+    const __half h = __float2half_rn(S[g]);
+    if (!__builtin_isfinite(__half2float(h))) *flag = 1;
+    const uint16_t bits = __half_as_ushort(h);
+    out[2 * g] = (uint8_t)bits;
+    out[2 * g + 1] = (uint8_t)(bits >> 8);
+  }
+}
+
+// Super-block layout: one 110-byte record per 256 weights,
+// [fp16 d][16 x 6-bit sc, LSB first][256 x 3-bit codes, LSB first].
+__global__ void k_pack_superblock(const uint8_t* codes, const uint16_t* D, const uint8_t* SC,
+                                  uint8_t* out, int64_t nrec) {
+  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < nrec;
+       r += (int64_t)gridDim.x * blockDim.x) {
+    uint8_t* o = out + r * 110;
+    o[0] = (uint8_t)D[r];
+    o[1] = (uint8_t)(D[r] >> 8);
+    uint64_t acc = 0;
+    int nbits = 0, pos = 2;
+    for (int j = 0; j < 16; ++j) {
+      acc |= (uint64_t)(SC[r * 16 + j] & 63u) << nbits;
+      nbits += 6;
+      while (nbits >= 8) { o[pos++] = (uint8_t)acc; acc >>= 8; nbits -= 8; }
+    }
+    for (int i = 0; i < 256; ++i) {
+      acc |= (uint64_t)(codes[r * 256 + i] & 7u) << nbits;
+      nbits += 3;
+      while (nbits >= 8) { o[pos++] = (uint8_t)acc; acc >>= 8; nbits -= 8; }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ state copies
+// Between the caller's coordinate-major layout (B, O, I, K) and the K planes.
+__global__ void k_state_io(float* inter, float* planar, int64_t N, int K, int to_planar) {
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < N;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    for (int k = 0; k < K; ++k) {
+      if (to_planar) planar[k * N + e] = inter[e * K + k];
+      else inter[e * K + k] = planar[k * N + e];
+    }
+  }
+}
+
+// Padded (B, Opad, Ipad) -> dense (B, O, I); elem_bytes is 2 or 4.
+__global__ void k_unpad(const uint8_t* src, uint8_t* dst, int64_t N, int64_t O, int64_t I,
+                        int64_t Opad, int64_t Ipad, int elem_bytes) {
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < N;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t row = e / I, col = e - row * I;
+    const int64_t b = row / O, o = row - b * O;
+    const int64_t si = (b * Opad + o) * Ipad + col;
+    if (elem_bytes == 4) reinterpret_cast<float*>(dst)[e] = reinterpret_cast<const float*>(src)[si];
+    else reinterpret_cast<uint16_t*>(dst)[e] = reinterpret_cast<const uint16_t*>(src)[si];
+  }
+}
+
+// ------------------------------------------------------------------ noise probe
+template <int K, bool kExact>
+__global__ void k_gumbel(uint64_t seed, int64_t e0, int64_t count, uint32_t t, float* out) {
+  for (int64_t n = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; n < count;
+       n += (int64_t)gridDim.x * blockDim.x) {
+    float g[K];
+    draw_gumbel<K, kExact>(g, seed, (uint64_t)(e0 + n), t);
+    for (int k = 0; k < K; ++k) out[n * K + k] = g[k];
+  }
+}
+
+dim3 flat_grid(int64_t n, int block = 256) {
+  int64_t g = (n + block - 1) / block;
+  if (g > 1 << 20) g = 1 << 20;
+  if (g < 1) g = 1;
+  return dim3((unsigned)g);
+}
+
+dim3 row_grid(const Layer& L) {
+  const int64_t gx = (L.I + kCols - 1) / kCols;
+  int64_t gy = (L.B * L.O + 3) / 4;
+  if (gy > 65535) gy = 65535;
+  return dim3((unsigned)gx, (unsigned)gy);
+}
+
+}  // namespace
+
+// ====================================================================== launchers
+ElemArgs base_args(const Layer& L) {
+  ElemArgs a{};
+  a.W = L.W;
+  a.G = L.G;
+  a.L = L.L; a.M = L.M; a.V = L.V;
+  a.S = L.S; a.MS = L.MS; a.VS = L.VS;
+  a.flag = L.flag;
+  a.N = L.N;
+  a.rows = (int32_t)(L.B * L.O);
+  a.O = (int32_t)L.O; a.I = (int32_t)L.I;
+  a.Opad = (int32_t)L.Opad; a.Ipad = (int32_t)L.Ipad;
+  a.gs = (int32_t)L.gs;
+  a.w_bf16 = L.w_bf16;
+  a.seed = L.cfg.seed;
+  for (int k = 0; k < 8; ++k) a.c[k] = k < L.K ? L.cfg.levels[k] : 0.f;
+  return a;
+}
+
+hipError_t launch_symmetrize_h(const float* Hin, void* Hout, int64_t B, int64_t I, int64_t Ipad,
+                               bool bf16, hipStream_t s) {
+  dim3 grid((unsigned)(Ipad / 32), (unsigned)(Ipad / 32), (unsigned)B);
+  hipLaunchKernelGGL(k_symmetrize, grid, dim3(32, 8), 0, s, Hin, Hout, I, Ipad, bf16 ? 1 : 0);
+  return hipGetLastError();
+}
+
+hipError_t launch_init_scales(const Layer& L, const float* scales_init, float cmax, hipStream_t s) {
+  if (L.cfg.layout == GSQ_LAYOUT_SUPERBLOCK) {
+    const int64_t nb = L.N / 256;
+    hipLaunchKernelGGL(k_init_scales_superblock, flat_grid(nb), dim3(256), 0, s, L.W, L.w_bf16, L.S,
+                       L.sb_d, L.sb_sc, nb, cmax);
+  } else if (scales_init) {
+    return hipMemcpyAsync(L.S, scales_init, L.NG * sizeof(float), hipMemcpyDeviceToDevice, s);
+  } else {
+    hipLaunchKernelGGL(k_init_scales_group, flat_grid(L.NG), dim3(256), 0, s, L.W, L.w_bf16, L.S,
+                       L.NG, (int)L.gs, cmax);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_init_logits(const Layer& L, const double* mids, hipStream_t s) {
+  InitConsts ic{};
+  for (int k = 0; k < 8; ++k) {
+    ic.c[k] = k < L.K ? L.cfg.levels[k] : 0.f;
+    ic.mids[k] = k + 1 < L.K ? mids[k] : 0.0;
+  }
+  ic.K = (int)L.K;
+  ic.alpha = L.cfg.alpha;
+  ic.sigma = L.cfg.sigma_init;
+  ic.noise = L.cfg.init_noise;
+  ic.seed = L.cfg.seed;
+  hipLaunchKernelGGL(k_init_logits, flat_grid(L.N), dim3(256), 0, s, L.W, L.w_bf16, L.S, L.L, L.N,
+                     (int)L.gs, ic);
+  return hipGetLastError();
+}
+
+template <int K>
+static hipError_t forward_k(const Layer& L, const ElemArgs& a, hipStream_t s) {
+  if (L.bf16) hipLaunchKernelGGL((k_forward<K, false>), row_grid(L), dim3(kBlock), 0, s, a);
+  else hipLaunchKernelGGL((k_forward<K, true>), row_grid(L), dim3(kBlock), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_forward(const Layer& L, const ElemArgs& a, hipStream_t s) {
+  switch (L.K) {
+    case 2: return forward_k<2>(L, a, s);
+    case 3: return forward_k<3>(L, a, s);
+    case 4: return forward_k<4>(L, a, s);
+    case 5: return forward_k<5>(L, a, s);
+    case 6: return forward_k<6>(L, a, s);
+    case 7: return forward_k<7>(L, a, s);
+    default: return forward_k<8>(L, a, s);
+  }
+}
+
+template <int K>
+static hipError_t backward_k(const Layer& L, const ElemArgs& a, bool sc, hipStream_t s) {
+  const dim3 g = row_grid(L), b(kBlock);
+  if (L.bf16) {
+    if (sc) hipLaunchKernelGGL((k_backward<K, false, true>), g, b, 0, s, a);
+    else hipLaunchKernelGGL((k_backward<K, false, false>), g, b, 0, s, a);
+  } else {
+    if (sc) hipLaunchKernelGGL((k_backward<K, true, true>), g, b, 0, s, a);
+    else hipLaunchKernelGGL((k_backward<K, true, false>), g, b, 0, s, a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_backward(const Layer& L, const ElemArgs& a, bool update_scales, hipStream_t s) {
+  switch (L.K) {
+    case 2: return backward_k<2>(L, a, update_scales, s);
+    case 3: return backward_k<3>(L, a, update_scales, s);
+    case 4: return backward_k<4>(L, a, update_scales, s);
+    case 5: return backward_k<5>(L, a, update_scales, s);
+    case 6: return backward_k<6>(L, a, update_scales, s);
+    case 7: return backward_k<7>(L, a, update_scales, s);
+    default: return backward_k<8>(L, a, update_scales, s);
+  }
+}
+
+hipError_t launch_harden(const Layer& L, uint8_t* codes, void* Rh, hipStream_t s) {
+  const ElemArgs a = base_args(L);
+  hipLaunchKernelGGL(k_harden, flat_grid(L.N), dim3(256), 0, s, a, (int)L.K,
+                     L.cfg.layout == GSQ_LAYOUT_SUPERBLOCK ? 1 : 0, L.bf16 ? 0 : 1, codes, Rh);
+  return hipGetLastError();
+}
+
+hipError_t launch_eff_scales(const Layer& L, float* out, hipStream_t s) {
+  hipLaunchKernelGGL(k_eff_scales, flat_grid(L.NG), dim3(256), 0, s, L.S, out, L.NG,
+                     L.cfg.layout == GSQ_LAYOUT_SUPERBLOCK ? 1 : 0, L.flag);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack(const Layer& L, const uint8_t* codes, uint8_t* out, hipStream_t s) {
+  if (L.cfg.layout == GSQ_LAYOUT_SUPERBLOCK) {
+    const int64_t nrec = L.N / 256;
+    hipLaunchKernelGGL(k_pack_superblock, flat_grid(nrec), dim3(256), 0, s, codes, L.sb_d, L.sb_sc,
+                       out, nrec);
+    return hipGetLastError();
+  }
+  const int b = L.K <= 2 ? 1 : L.K <= 4 ? 2 : 3;
+  const int64_t n8 = L.N / 8;
+  hipLaunchKernelGGL(k_pack_codes, flat_grid(n8), dim3(256), 0, s, codes, out, n8, b);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  hipLaunchKernelGGL(k_pack_scales, flat_grid(L.NG), dim3(256), 0, s, L.S, out + L.N * b / 8, L.NG,
+                     L.flag);
+  return hipGetLastError();
+}
+
+hipError_t launch_state_io(const Layer& L, float* inter, float* planar, bool to_planar,
+                           hipStream_t s) {
+  hipLaunchKernelGGL(k_state_io, flat_grid(L.N), dim3(256), 0, s, inter, planar, L.N, (int)L.K,
+                     to_planar ? 1 : 0);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_residual(const Layer& L, const void* Rpad, void* out, hipStream_t s) {
+  hipLaunchKernelGGL(k_unpad, flat_grid(L.N), dim3(256), 0, s, static_cast<const uint8_t*>(Rpad),
+                     static_cast<uint8_t*>(out), L.N, L.O, L.I, L.Opad, L.Ipad, L.bf16 ? 2 : 4);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_grad(const Layer& L, const float* Gpad, float* out, hipStream_t s) {
+  hipLaunchKernelGGL(k_unpad, flat_grid(L.N), dim3(256), 0, s,
+                     reinterpret_cast<const uint8_t*>(Gpad), reinterpret_cast<uint8_t*>(out), L.N,
+                     L.O, L.I, L.Opad, L.Ipad, 4);
+  return hipGetLastError();
+}
+
+template <int K>
+static hipError_t gumbel_k(const gsq_config& cfg, int64_t e0, int64_t count, int64_t t, float* out,
+                           hipStream_t s) {
+  if (cfg.precision == GSQ_PREC_BF16)
+    hipLaunchKernelGGL((k_gumbel<K, false>), flat_grid(count), dim3(256), 0, s, cfg.seed, e0, count,
+                       (uint32_t)t, out);
+  else
+    hipLaunchKernelGGL((k_gumbel<K, true>), flat_grid(count), dim3(256), 0, s, cfg.seed, e0, count,
+                       (uint32_t)t, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_gumbel(const gsq_config& cfg, int64_t e0, int64_t count, int64_t t, float* out,
+                         hipStream_t s) {
+  switch (cfg.n_levels) {
+    case 2: return gumbel_k<2>(cfg, e0, count, t, out, s);
+    case 3: return gumbel_k<3>(cfg, e0, count, t, out, s);
+    case 4: return gumbel_k<4>(cfg, e0, count, t, out, s);
+    case 5: return gumbel_k<5>(cfg, e0, count, t, out, s);
+    case 6: return gumbel_k<6>(cfg, e0, count, t, out, s);
+    case 7: return gumbel_k<7>(cfg, e0, count, t, out, s);
+    default: return gumbel_k<8>(cfg, e0, count, t, out, s);
+  }
+}
+
+}  // namespace gsq

@@ -1,0 +1,90 @@
+// Internal declarations shared by the host API and the kernel launchers.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "gsq.h"
+
+namespace gsq {
+
+constexpr int kTileM = 128;   // contraction tile (rows of R / G)
+constexpr int kTileN = 128;   // contraction tile (columns of G = rows of H)
+constexpr int kPadK = 128;    // padding of the inner dimension (H is padded with zeros)
+
+// Everything an elementwise kernel needs, passed by value.
+struct ElemArgs {
+  const void* W;        // B*O*I, fp32 or bf16
+  const float* G;       // B*Opad*Ipad fp32
+  void* Rout;           // B*Opad*Ipad, fp32 (FP32 path) or bf16
+  float *L, *M, *V;     // K planes of N fp32 each
+  float *S, *MS, *VS;   // one per scale group
+  int* flag;            // sticky non-finite flag
+  int64_t N;            // B*O*I
+  int32_t rows;         // B*O
+  int32_t O, I, Opad, Ipad, gs, w_bf16;
+  uint64_t seed;
+  float c[8];
+  // this step's sample
+  uint32_t t;
+  int32_t noise;
+  float kappa, inv_tau;       // fp32 path of the BF16 precision
+  double inv_tau_d;           // fp64 path of the FP32 precision
+  // Adam
+  float lr, lr_s, b1, b2, eps, step_l, step_s, rbc2;  // step_* = lr / (1 - b1^n), rbc2 = 1/sqrt(1 - b2^n)
+  double step_l_d, step_s_d, rbc2_d;
+  // sample of the next step, drawn by the backward kernel when fuse != 0
+  int32_t fuse;
+  uint32_t t_next;
+  float kappa_n, inv_tau_n;
+  double inv_tau_n_d;
+};
+
+struct Layer {
+  gsq_config cfg;
+  int64_t B, O, I, K, gs, Opad, Ipad, N, NG;
+  bool bf16;        // precision == GSQ_PREC_BF16
+  int w_bf16;
+  void* W = nullptr;
+  void* H = nullptr;
+  float *L = nullptr, *M = nullptr, *V = nullptr;
+  float *S = nullptr, *MS = nullptr, *VS = nullptr;
+  void* R[2] = {nullptr, nullptr};
+  float* G = nullptr;
+  double* partials = nullptr;
+  int64_t tiles_per_batch = 0;
+  int* flag = nullptr;
+  uint16_t* sb_d = nullptr;
+  uint8_t* sb_sc = nullptr;
+  uint8_t* codes = nullptr;
+  int64_t t = 0;
+  int cur = 0;            // R buffer holding a prepared sample (when r_valid)
+  bool r_valid = false;
+  int64_t r_t = -1;
+  float r_tau = 0.f, r_kappa = 0.f;
+  int r_noise = 0;
+  int last = -1;          // R buffer of the most recent step (-1: none)
+};
+
+// ---- launchers (gsq_elem.hip)
+hipError_t launch_symmetrize_h(const float* Hin, void* Hout, int64_t B, int64_t I, int64_t Ipad,
+                               bool bf16, hipStream_t s);
+hipError_t launch_init_scales(const Layer& L, const float* scales_init, float cmax, hipStream_t s);
+hipError_t launch_init_logits(const Layer& L, const double* mids, hipStream_t s);
+hipError_t launch_forward(const Layer& L, const ElemArgs& a, hipStream_t s);
+hipError_t launch_backward(const Layer& L, const ElemArgs& a, bool update_scales, hipStream_t s);
+hipError_t launch_harden(const Layer& L, uint8_t* codes, void* Rh, hipStream_t s);
+hipError_t launch_eff_scales(const Layer& L, float* out, hipStream_t s);
+hipError_t launch_pack(const Layer& L, const uint8_t* codes, uint8_t* out, hipStream_t s);
+hipError_t launch_state_io(const Layer& L, float* inter, float* planar, bool to_planar, hipStream_t s);
+hipError_t launch_copy_residual(const Layer& L, const void* Rpad, void* out, hipStream_t s);
+hipError_t launch_copy_grad(const Layer& L, const float* Gpad, float* out, hipStream_t s);
+hipError_t launch_gumbel(const gsq_config& cfg, int64_t e0, int64_t count, int64_t t, float* out,
+                         hipStream_t s);
+ElemArgs base_args(const Layer& L);
+
+// ---- launchers (gsq_contract.hip)
+int64_t contract_tiles_per_batch(const Layer& L);
+hipError_t launch_contract(const Layer& L, const void* R, bool want_loss, hipStream_t s);
+hipError_t launch_reduce_loss(const Layer& L, float* loss_out, hipStream_t s);
+
+}  // namespace gsq

@@ -1,0 +1,335 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle on the same seeded inputs.
+
+Tolerances (max |gpu - oracle| / max |oracle| per tensor): 1e-5 for the FP32 precision
+(fp32 operands, fp64 accumulation and elementwise arithmetic) and 1e-3 for the BF16
+precision (bf16 operands on the matrix cores, fp32 elementwise arithmetic); integer
+results (codes, packed bytes, RTN codes) must be bit-exact.
+"""
+import numpy as np
+import pytest
+
+from oracle import gsq as ref
+from oracle import pack as refpack
+from oracle import philox
+from paper_2604_18556_amd import binding as B
+from paper_2604_18556_amd import inputs
+
+from gpu_common import Pair, assert_state_close, oracle_params, rel_err
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+TOL = {"fp32": 1e-5, "bf16": 1e-3}
+L3, L4, L8 = inputs.L3, inputs.L4, inputs.L8
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.load()
+    return torch.device("cuda:0")
+
+
+def layer_inputs(O, I, batch=1, bf16=True, seed=0, tokens=None):
+    rng = np.random.default_rng(100 + seed)
+    W = rng.normal(0, 0.02, (batch, O, I)).astype(np.float32)
+    W.reshape(-1)[rng.choice(W.size, max(1, W.size // 1000), replace=False)] *= 10
+    if bf16:
+        W = inputs.to_bf16_values(W)
+    Hs = []
+    for b in range(batch):
+        X = rng.standard_t(4, (tokens or 2 * I, I)) * rng.lognormal(0, 0.5, I)
+        Hs.append((X.T @ X).astype(np.float32))
+    return W, np.stack(Hs)
+
+
+# ------------------------------------------------------------------ noise
+@pytest.mark.parametrize("K", [3, 4, 8])
+def test_gumbel_fp32_path_is_bit_exact(dev, K):
+    cfg = B.LayerConfig(4, 256, tuple(range(K)), 128, precision=B.PREC_FP32, seed=12345678901)
+    n = 200_000
+    out = torch.empty(n, K, device=dev)
+    B.gumbel(cfg, 7 * 2**32 - 1000, n, 17, out)
+    want = philox.gumbel(12345678901, np.arange(7 * 2**32 - 1000, 7 * 2**32 - 1000 + n), 17, K)
+    got = out.cpu().numpy().astype(np.float64)
+    mism = np.count_nonzero(got != want)
+    # both round -ln(-ln u) from fp64 to fp32; only an fp64 value within 1e-16 of a rounding
+    # boundary could round differently
+    assert mism <= 2, f"{mism} mismatches"
+
+
+def test_gumbel_bf16_path_is_close(dev):
+    cfg = B.LayerConfig(4, 256, L8, 128, precision=B.PREC_BF16, seed=3)
+    n = 400_000
+    out = torch.empty(n, 8, device=dev)
+    B.gumbel(cfg, 0, n, 2, out)
+    want = philox.gumbel(3, np.arange(n), 2, 8)
+    err = np.abs(out.cpu().numpy() - want)
+    print(f"bf16-path Gumbel: max abs error {err.max():.3e}, mean {err.mean():.3e}")
+    # hardware log2 twice: error of a few float32 ulps of -ln u, which becomes absolute in g
+    assert err.max() < 2e-5, err.max()
+
+
+# ------------------------------------------------------------------ initialisation
+@pytest.mark.parametrize("prec,O,I,K,gs", [("fp32", 256, 256, 4, 128), ("bf16", 200, 384, 3, 128),
+                                           ("bf16", 64, 512, 8, 64), ("bf16", 33, 272, 5, 16)])
+def test_init_matches_oracle(dev, prec, O, I, K, gs):
+    levels = {3: L3, 4: L4, 5: (-2.0, -1.0, 0.0, 1.0, 2.0), 8: L8}[K]
+    W, H = layer_inputs(O, I, bf16=prec == "bf16", seed=K)
+    rcfg = ref.Config(O, I, levels, gs, precision=prec, seed=99, sigma_init=0.7)
+    pair = Pair(rcfg, W, H, dev)
+    st = ref.init_layer(rcfg, W)
+    got = pair.get()
+    np.testing.assert_array_equal(got.scales, st.scales)        # IEEE fp32 division on both sides
+    assert rel_err(got.logits, st.logits) <= 1e-6
+    assert np.all(got.m == 0) and np.all(got.v == 0) and got.t == 0
+    # noise-free prior: the argmax of the initial logits is the round-to-nearest code
+    rcfg0 = ref.Config(O, I, levels, gs, precision=prec, init_noise=False)
+    pair0 = Pair(rcfg0, W, H, dev)
+    codes = torch.empty(1, O, I, dtype=torch.uint8, device=dev)
+    pair0.layer.harden(codes=codes)
+    np.testing.assert_array_equal(codes.cpu().numpy(), ref.init_layer(rcfg0, W).extra["q0"])
+
+
+def test_superblock_init_matches_oracle(dev):
+    W, H = layer_inputs(48, 512, batch=3, seed=5)
+    W[0, 0, :16] = 0.0
+    rcfg = ref.Config(48, 512, L8, layout="superblock", batch=3, precision="bf16", seed=1)
+    pair = Pair(rcfg, W, H, dev)
+    st = ref.init_layer(rcfg, W)
+    got = pair.get()
+    np.testing.assert_array_equal(got.scales, st.scales)
+    assert rel_err(got.logits, st.logits) <= 1e-6
+
+
+# ------------------------------------------------------------------ one step from a shared state
+def _warm(st, rng):
+    """A state with non-zero Adam moments (as after some steps)."""
+    st = st.copy()
+    st.m = (rng.standard_normal(st.m.shape) * 1e-3).astype(np.float32)
+    st.v = (rng.uniform(0.5, 2, st.v.shape) * 1e-6).astype(np.float32)
+    st.m_s = (rng.standard_normal(st.m_s.shape) * 1e-4).astype(np.float32)
+    st.v_s = (rng.uniform(0.5, 2, st.v_s.shape) * 1e-8).astype(np.float32)
+    st.t = 7
+    return st
+
+
+CASES = [
+    # precision, batch, O, I, K, gs, layout, tau, kappa
+    ("fp32", 1, 256, 256, 4, 128, "group", 0.05, 1.0),
+    ("fp32", 1, 256, 256, 4, 128, "group", 1.0, 1.0),
+    ("fp32", 2, 70, 384, 3, 64, "group", 0.3, 2.0),
+    ("bf16", 1, 200, 384, 3, 128, "group", 0.05, 1.0),
+    ("bf16", 1, 200, 384, 3, 128, "group", 1.0, 1.0),
+    ("bf16", 1, 130, 512, 8, 128, "group", 0.2, 1.0),
+    ("bf16", 1, 96, 256, 4, 64, "group", 0.5, 3.0),
+    ("bf16", 3, 40, 512, 8, 16, "superblock", 0.3, 1.0),
+]
+
+
+@pytest.mark.parametrize("prec,batch,O,I,K,gs,layout,tau,kappa", CASES)
+@pytest.mark.parametrize("warm", [False, True])
+def test_single_step_matches_oracle(dev, prec, batch, O, I, K, gs, layout, tau, kappa, warm):
+    levels = {3: L3, 4: L4, 8: L8}[K]
+    W, H = layer_inputs(O, I, batch=batch, bf16=prec == "bf16", seed=O + I)
+    rcfg = ref.Config(O, I, levels, gs, batch=batch, layout=layout, precision=prec, seed=4)
+    pair = Pair(rcfg, W, H, dev)
+    st = ref.init_layer(rcfg, W)
+    if warm:
+        st = _warm(st, np.random.default_rng(O))
+    pair.put(st)
+    lr_s = 0.0 if layout == "superblock" else 5e-5
+    prm = B.StepParams(tau=tau, kappa=kappa, lr_scales=lr_s)
+    loss = pair.step(prm)
+    R, G = pair.intermediates()
+    new, L, inter = ref.step(rcfg, W, pair.Hs, st, oracle_params(prm), want=True)
+    tol = TOL[prec]
+    assert np.all(np.abs(loss - L) <= tol * np.abs(L)), (loss, L)
+    assert rel_err(G, inter["G"]) <= tol, rel_err(G, inter["G"])
+    if prec == "fp32":
+        assert rel_err(R, inter["R"]) <= tol
+    else:
+        # R is stored in bf16 on both sides, rounded from the GPU's fp32 value and the oracle's
+        # fp64 value: they agree to one bf16 ulp of the largest magnitude (2^-7 relative)
+        assert rel_err(R, inter["R"]) <= 2.0**-7, rel_err(R, inter["R"])
+    got = pair.get()
+    assert_state_close(got, new, inter["G"], tol, st.t + 1, label=f"{prec} {O}x{I} K{K}")
+    if not warm:
+        # from zero moments m = (1 - beta1) d: the logit and scale gradients themselves
+        d_gpu = got.m / (1 - np.float32(0.9))
+        assert rel_err(d_gpu, inter["dlogits"]) <= tol
+        if lr_s > 0:
+            assert rel_err(got.m_s / (1 - np.float32(0.9)), inter["dscales"]) <= tol
+
+
+# ------------------------------------------------------------------ harden / pack
+@pytest.mark.parametrize("K,gs,layout", [(4, 128, "group"), (3, 64, "group"), (8, 128, "group"),
+                                         (2, 16, "group"), (8, 16, "superblock")])
+def test_harden_and_pack_are_bit_exact(dev, K, gs, layout):
+    levels = {2: (-0.5, 0.5), 3: L3, 4: L4, 8: L8}[K]
+    O, I, batch = 37, 512, 2
+    W, H = layer_inputs(O, I, batch=batch, seed=K)
+    rcfg = ref.Config(O, I, levels, gs, batch=batch, layout=layout, precision="bf16", seed=2)
+    pair = Pair(rcfg, W, H, dev)
+    st = ref.init_layer(rcfg, W)
+    rng = np.random.default_rng(K)
+    st.logits = rng.integers(-3, 4, st.logits.shape).astype(np.float32)   # many exact ties
+    if layout == "group":
+        st.scales = (st.scales * rng.uniform(0.5, 2, st.scales.shape)).astype(np.float32)
+    pair.put(st)
+    codes = torch.empty(batch, O, I, dtype=torch.uint8, device=dev)
+    scales = torch.empty(st.scales.shape, device=dev)
+    hl = torch.empty(batch, device=dev)
+    pair.layer.harden(codes=codes, scales=scales, hard_loss=hl)
+    c_ref, s_ref, hl_ref = ref.harden_layer(rcfg, W, pair.Hs, st)
+    np.testing.assert_array_equal(codes.cpu().numpy(), c_ref)
+    np.testing.assert_array_equal(scales.cpu().numpy(), s_ref)
+    assert np.all(np.abs(hl.cpu().numpy() - hl_ref) <= 1e-3 * np.abs(hl_ref))
+    packed = torch.empty(B.packed_size(pair.bcfg), dtype=torch.uint8, device=dev)
+    pair.layer.pack(packed)
+    if layout == "group":
+        expect = refpack.pack_plain(c_ref, ref.scales_fp16(st.scales), K, gs)
+    else:
+        sd, ssc, _ = ref.superblock_scales(W.astype(np.float64), rcfg)
+        expect = refpack.pack_superblock(c_ref, sd, ssc)
+    np.testing.assert_array_equal(packed.cpu().numpy(), expect)
+
+
+# ------------------------------------------------------------------ trajectory (tiny fp32 layer)
+@pytest.mark.parametrize("fused", [False, True])
+def test_tiny_layer_trajectory(dev, fused):
+    """100 Adam steps on the 256 x 256 fp32 layer, tau 1.0 -> 0.05: codes and packed bytes equal."""
+    w = inputs.WORKLOADS["tiny-256x256-k4"]
+    W, H = inputs.make_layer(w)
+    rcfg = ref.Config(256, 256, w.levels, 128, precision="fp32", seed=0)
+    pair = Pair(rcfg, W, H, dev)
+    st = ref.init_layer(rcfg, W)
+    T = w.steps
+    losses_gpu, losses_ref = [], []
+    for t in range(T):
+        tau = ref.tau_schedule(t, T)
+        nxt = ref.tau_schedule(t + 1, T) if (fused and t + 1 < T) else 0.0
+        prm = B.StepParams(tau=tau, tau_next=nxt)
+        losses_gpu.append(pair.step(prm)[0])
+        st, L = ref.step(rcfg, W, pair.Hs, st, oracle_params(prm))
+        losses_ref.append(L[0])
+    lg, lr_ = np.array(losses_gpu), np.array(losses_ref)
+    assert np.all(np.abs(lg - lr_) <= 1e-5 * np.abs(lr_)), np.abs(lg - lr_).max()
+    got = pair.get()
+    c_gpu, c_ref = ref.harden(got.logits), ref.harden(st.logits)
+    diff = np.argwhere(c_gpu != c_ref)
+    srt = np.sort(st.logits, -1)
+    gap = srt[..., -1] - srt[..., -2]
+    for idx in diff:   # admissible only where the oracle's own top-2 gap is a float-order tie
+        assert gap[tuple(idx)] < 1e-4 * np.abs(st.logits).max(), idx
+    if not len(diff):
+        packed = torch.empty(B.packed_size(pair.bcfg), dtype=torch.uint8, device=dev)
+        pair.layer.pack(packed)
+        np.testing.assert_array_equal(packed.cpu().numpy(),
+                                      refpack.pack_plain(c_ref, ref.scales_fp16(st.scales), 4, 128))
+
+
+def test_fused_and_unfused_steps_are_identical(dev):
+    W, H = layer_inputs(150, 384, seed=9)
+    rcfg = ref.Config(150, 384, L8, 128, precision="bf16", seed=8)
+    a, b = Pair(rcfg, W, H, dev), Pair(rcfg, W, H, dev)
+    for t in range(6):
+        tau = 1.0 - 0.15 * t
+        a.step(B.StepParams(tau=tau, kappa=1.0 + t, tau_next=tau - 0.15, kappa_next=2.0 + t))
+        b.step(B.StepParams(tau=tau, kappa=1.0 + t))
+    sa, sb = a.get(), b.get()
+    for k in ("logits", "m", "v", "scales", "m_s", "v_s"):
+        np.testing.assert_array_equal(getattr(sa, k), getattr(sb, k))
+
+
+# ------------------------------------------------------------------ determinism and resume
+def test_determinism_and_exact_resume(dev):
+    W, H = layer_inputs(128, 512, seed=11)
+    rcfg = ref.Config(128, 512, L4, 128, precision="bf16", seed=21)
+    sched = [B.StepParams(tau=1.0 - 0.09 * t, tau_next=(1.0 - 0.09 * (t + 1)) if t < 9 else 0.0)
+             for t in range(10)]
+    a, b = Pair(rcfg, W, H, dev), Pair(rcfg, W, H, dev)
+    for p in sched:
+        a.step(p)
+        b.step(p)
+    sa, sb = a.get(), b.get()
+    for k in ("logits", "m", "v", "scales"):
+        np.testing.assert_array_equal(getattr(sa, k), getattr(sb, k))
+    c = Pair(rcfg, W, H, dev)
+    for p in sched[:5]:
+        c.step(p)
+    mid = c.get()
+    d = Pair(rcfg, W, H, dev)
+    d.put(mid)
+    for p in sched[5:]:
+        d.step(p)
+    sd = d.get()
+    for k in ("logits", "m", "v", "scales", "m_s", "v_s"):
+        np.testing.assert_array_equal(getattr(sd, k), getattr(sa, k))
+    assert sd.t == sa.t == 10
+
+
+# ------------------------------------------------------------------ failure reporting
+def test_non_finite_weights_are_reported(dev):
+    W, H = layer_inputs(32, 256, seed=1)
+    W[0, 3, 5] = np.inf
+    rcfg = ref.Config(32, 256, L4, 128, precision="bf16")
+    pair = Pair(rcfg, W, H, dev)
+    pair.step(B.StepParams(tau=0.5))
+    with pytest.raises(B.GsqError) as e:
+        pair.layer.check()
+    assert e.value.status == B.GSQ_ENONFINITE
+    with pytest.raises(B.GsqError):
+        pair.layer.step(B.StepParams(tau=0.0))
+    with pytest.raises(B.GsqError) as e:
+        pair.layer.step(B.StepParams(tau=0.5, lr_scales=1e-3, beta1=1.0))
+    assert e.value.status == B.GSQ_EINVAL
+
+
+def test_superblock_rejects_scale_training(dev):
+    W, H = layer_inputs(16, 256, seed=2)
+    rcfg = ref.Config(16, 256, L8, layout="superblock", precision="bf16")
+    pair = Pair(rcfg, W, H, dev)
+    with pytest.raises(B.GsqError) as e:
+        pair.layer.step(B.StepParams(tau=0.5, lr_scales=1e-5))
+    assert e.value.status == B.GSQ_EUNSUPPORTED
+
+
+# ------------------------------------------------------------------ full size, sampled rows
+def test_full_size_attention_layer_on_sampled_rows(dev):
+    """The 4096 x 4096 ternary attention projection in the benchmark's launch configuration
+    (next sample drawn by the backward pass): init, two steps, sampled rows vs the oracle."""
+    w = inputs.WORKLOADS["attn-4096x4096-k3"]
+    W, Hd = inputs.make_layer(w, device=dev)
+    H = Hd.cpu().numpy()
+    rcfg = ref.Config(w.out_features, w.in_features, w.levels, w.group_size, precision="bf16", seed=0)
+    pair_cfg = B.LayerConfig(w.out_features, w.in_features, w.levels, w.group_size,
+                             precision=B.PREC_BF16, seed=0)
+    layer = B.Layer(pair_cfg, torch.from_numpy(W).to(dev).to(torch.bfloat16), Hd)
+    rows = np.array([0, 1, 777, 2048, 4095])
+    Hs = ref.symmetrize(H)
+    st = ref.init_layer(rcfg, W, rows=rows)
+    O, I, K = w.out_features, w.in_features, 3
+    lg = torch.empty(1, O, I, K, device=dev)
+    sc = torch.empty(1, O, I // 128, device=dev)
+    layer.get_state(logits=lg, scales=sc)
+    np.testing.assert_array_equal(sc.cpu().numpy()[:, rows], st.scales)
+    assert rel_err(lg.cpu().numpy()[:, rows], st.logits) <= 1e-6
+    T = w.steps
+    for t in range(2):
+        tau, nxt = ref.tau_schedule(t, T), ref.tau_schedule(t + 1, T)
+        prm = B.StepParams(tau=tau, tau_next=nxt)
+        loss = torch.zeros(1, device=dev)
+        layer.step(prm, loss_out=loss)
+        G = torch.empty(1, O, I, device=dev)
+        layer.intermediates(grad=G)
+        st_new, _, inter = ref.step(rcfg, W, Hs, st, oracle_params(prm), rows=rows, want=True)
+        assert rel_err(G.cpu().numpy()[:, rows], inter["G"]) <= 1e-3
+        got = {k: torch.empty(1, O, I, K, device=dev) for k in ("logits", "m", "v")}
+        got.update({k: torch.empty(1, O, I // 128, device=dev) for k in ("scales", "m_s", "v_s")})
+        tt = layer.get_state(**got)
+        gst = ref.State(*(got[k].cpu().numpy()[:, rows] for k in ("logits", "m", "v", "scales", "m_s", "v_s")), tt)
+        assert_state_close(gst, st_new, inter["G"], 1e-3, t + 1, label=f"full-size step {t}")
+        assert np.isfinite(loss.item()) and loss.item() > 0
+        st = st_new
