@@ -1,0 +1,261 @@
+#!/usr/bin/env python3
+"""GSQ layer-step benchmark on one MI355X.
+
+A step is one full pass of the hot path over one layer: Philox Gumbel noise, the tempered
+softmax sample and residual (Alg. 1), the contraction P = R H with the loss (Eq. 1), the
+gradient of logits and scales, and the Adam update.  The default workload is the 8B-class
+ternary attention projection (W 4096 x 4096, bf16, K = 3 levels {-1, 0, 1}, groups of 128,
+H from 4096 heavy-tailed synthetic tokens), stepped with the paper's linear temperature
+schedule 1.0 -> 0.05 over 500 steps.  Inputs are seeded and synthetic and resident in HBM
+before timing starts.
+
+Prints one JSON line: steps/s, the roofline of the dominant kernel (its duration measured
+with HIP events on the library's stream during the timed steps), and the CPU oracle timed
+on a bounded sample of the same workload.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+    python bench.py --copy-calibration   # plain device copy of known size, for PMC scaling
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "GSQ steps/sec per layer (fwd+bwd+update) + % HBM / MFMA peak, 1 MI355X"
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+PEAK_BF16_TFLOPS = 2500.0      # dense bf16 MFMA
+PEAK_FP64_TFLOPS = 78.6        # fp64 vector (the FP32 precision accumulates in fp64)
+DEFAULT_WORKLOAD = "attn-4096x4096-k3"
+
+
+def algorithmic_work(w, fused, want_loss, lr_scales):
+    """Per-launch algorithmic bytes / flops of each step kernel (see the design notes).
+
+    Per coordinate, bf16 W and R, fp32 logits / moments / gradient, K levels, groups of gs:
+      forward   4K (logits) + 2 (W) + 2 (R)                      + 4/gs (scale)
+      backward  12K read + 12K write (logits, m, v) + 4 (G)      + scale state
+                + [fused] 2 (W) + 2 (next R)
+      contract  2 O I^2 flops per layer
+    """
+    B, O, I, K, gs = w.batch, w.out_features, w.in_features, len(w.levels), w.group_size
+    if w.layout == "superblock":
+        gs = 16
+    n = B * O * I
+    wb = 2 if w.precision == "bf16" else 4
+    scale_b = (24.0 if lr_scales > 0 else 4.0) / gs
+    fwd = n * (4 * K + 2 * wb + 4.0 / gs)
+    bwd = n * (24 * K + 4 + scale_b + (2 * wb if fused else 0))
+    flops = 2.0 * B * O * I * I
+    contract_bytes = n * (wb + 4 + (wb if want_loss else 0)) + B * I * I * wb
+    return {"forward": ("hbm", fwd), "backward": ("hbm", bwd), "contract": ("flops", flops, contract_bytes)}
+
+
+def source_sha(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch from the committed PMC summary, if it matches the current source."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path)).get(f"{kernel}:{workload}")
+    except (ValueError, OSError):
+        return None
+    if not rec:
+        return None
+    src = os.path.join(ROOT, "paper_2604_18556_amd", "csrc", rec["source"])
+    if not os.path.exists(src) or source_sha(src) != rec["source_sha256"]:
+        return None
+    return rec["bytes_per_launch"]
+
+
+def cpu_baseline(w, W, H, rows, steps, lr_scales):
+    """The oracle, untuned, on ``rows`` rows of the layer for ``steps`` steps (host cores)."""
+    import numpy as np
+    from oracle import gsq as ref
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count()
+    rcfg = ref.Config(w.out_features, w.in_features, w.levels, w.group_size, batch=w.batch,
+                      layout=w.layout, precision=w.precision, seed=0)
+    sel = np.arange(min(rows, w.out_features))
+    Hs = ref.symmetrize(H)
+    st = ref.init_layer(rcfg, W, rows=sel)
+    t0 = time.perf_counter()
+    for t in range(steps):
+        prm = ref.StepParams(tau=ref.tau_schedule(t, w.steps), lr_scales=lr_scales)
+        st, _ = ref.step(rcfg, W, Hs, st, prm, rows=sel)
+    sec = (time.perf_counter() - t0) / steps
+    frac = len(sel) / w.out_features
+    return {"value": frac / sec, "unit": "steps/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{len(sel)} of {w.out_features} rows x {steps} steps "
+                      f"({sec:.2f} s/step), scaled to the whole layer by the row fraction",
+            "cpu_count": os.cpu_count()}
+
+
+def copy_calibration(dev, gib=1):
+    import torch
+    n = gib * (1 << 30) // 4
+    src = torch.ones(n, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 5}))
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=500)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--loss-every", type=int, default=1, help="request the loss every n steps")
+    ap.add_argument("--no-fuse", action="store_true", help="do not draw the next sample in the backward pass")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=512)
+    ap.add_argument("--cpu-steps", type=int, default=3)
+    ap.add_argument("--copy-calibration", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU: the GSQ layer step is measured per GPU and this build has "
+              f"no multi-GPU path (asked for --gpus {args.gpus})", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2604_18556_amd import binding as B
+    from paper_2604_18556_amd import inputs
+
+    dev = torch.device("cuda:0")
+    if args.copy_calibration:
+        copy_calibration(dev)
+        return
+
+    w = inputs.WORKLOADS[args.workload]
+    W, Hd = inputs.make_layer(w, device=dev)
+    Wd = torch.from_numpy(W).to(dev)
+    if w.precision == "bf16":
+        Wd = Wd.to(torch.bfloat16)
+    cfg = B.LayerConfig(w.out_features, w.in_features, w.levels, w.group_size, w.batch,
+                        B.LAYOUT_SUPERBLOCK if w.layout == "superblock" else B.LAYOUT_GROUP,
+                        B.PREC_BF16 if w.precision == "bf16" else B.PREC_FP32, seed=0)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    layer = B.Layer(cfg, Wd, Hd)
+    torch.cuda.synchronize()
+    init_ms = (time.perf_counter() - t0) * 1e3
+
+    T = w.steps
+    fused = not args.no_fuse
+    loss = torch.zeros(w.batch, device=dev)
+
+    def tau_at(t):
+        t %= T
+        return 1.0 + (0.05 - 1.0) * t / (T - 1)
+
+    def run(t0, n):
+        for i in range(n):
+            t = t0 + i
+            p = B.StepParams(tau=tau_at(t), lr_scales=w.lr_scales,
+                             tau_next=tau_at(t + 1) if fused else 0.0)
+            layer.step(p, loss_out=loss if (t % args.loss_every == 0) else None)
+
+    run(0, args.warmup)
+    torch.cuda.synchronize()
+    layer.timing(True)
+    layer.timing_read(reset=True)
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    run(args.warmup, args.steps)
+    end.record()
+    torch.cuda.synchronize()
+    ms_total = start.elapsed_time(end)
+    kern = layer.timing_read(reset=True)
+    layer.timing(False)
+    layer.check()
+    ms_step = ms_total / args.steps
+
+    # once per layer: harden (+ hard loss) and pack
+    codes = torch.empty(w.batch, w.out_features, w.in_features, dtype=torch.uint8, device=dev)
+    hl = torch.empty(w.batch, device=dev)
+    packed = torch.empty(B.packed_size(cfg), dtype=torch.uint8, device=dev)
+    layer.timing(True)
+    layer.harden(codes=codes, hard_loss=hl)
+    layer.pack(packed)
+    once = layer.timing_read(reset=True)
+    layer.timing(False)
+
+    work = algorithmic_work(w, fused, args.loss_every == 1, w.lr_scales)
+    per_kernel = {}
+    for name, (ms, cnt) in kern.items():
+        if cnt == 0:
+            continue
+        avg = ms / cnt
+        entry = {"launches": cnt, "avg_ms": avg, "ms_per_step": ms / args.steps}
+        if name in ("forward", "backward"):
+            gbs = work[name][1] / (avg * 1e-3) / 1e9
+            entry.update(bound="hbm", achieved=gbs, peak=PEAK_HBM_GBS, unit="GB/s",
+                         frac=gbs / PEAK_HBM_GBS, bytes_per_launch=work[name][1])
+        elif name == "contract":
+            tf = work[name][1] / (avg * 1e-3) / 1e12
+            peak = PEAK_BF16_TFLOPS if w.precision == "bf16" else PEAK_FP64_TFLOPS
+            entry.update(bound="mfma" if w.precision == "bf16" else "alu", achieved=tf, peak=peak,
+                         unit="TFLOP/s", frac=tf / peak, flops_per_launch=work[name][1])
+        per_kernel[name] = entry
+    dom = max((k for k in per_kernel if "bound" in per_kernel[k]), key=lambda k: per_kernel[k]["ms_per_step"])
+    d = per_kernel[dom]
+    src = {"forward": "gsq_elem.hip", "backward": "gsq_elem.hip", "contract": "gsq_contract.hip"}[dom]
+    roofline = {"bound": d["bound"], "achieved": d["achieved"], "peak": d["peak"], "unit": d["unit"],
+                "frac": d["frac"], "traffic": measured_traffic(dom, w.name), "kernel": dom,
+                "avg_ms": d["avg_ms"], "source": src}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, W, Hd.cpu().numpy(), args.cpu_rows, args.cpu_steps, w.lr_scales)
+
+    out = {
+        "metric": METRIC,
+        "value": 1e3 / ms_step,
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.precision == "bf16" else "fp32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": w.batch, "out_features": w.out_features,
+                   "in_features": w.in_features, "levels": len(w.levels), "group_size": w.group_size,
+                   "layout": w.layout, "precision": w.precision, "calibration_tokens": w.tokens,
+                   "tau_schedule": f"linear 1.0 -> 0.05 over {T} steps", "optimizer": "adam",
+                   "next_sample_fused": fused, "loss_every": args.loss_every, "parallelism": "none"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "kernels": per_kernel,
+        "once_per_layer": {"init_ms": init_ms,
+                           "harden_ms": once["harden"][0], "pack_ms": once["pack"][0],
+                           "hard_loss_contract_ms": once["contract"][0]},
+        "gpu_vs_cpu": None if cpu is None else (1e3 / ms_step) / cpu["value"],
+    }
+    print(json.dumps(out), flush=True)
+    layer.destroy()
+
+
+if __name__ == "__main__":
+    main()

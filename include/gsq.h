@@ -171,6 +171,30 @@ gsq_status gsq_get_intermediates(gsq_layer* h, void* residual, float* grad, hipS
 gsq_status gsq_gumbel(const gsq_config* cfg, int64_t e0, int64_t count, int64_t t, float* g_out,
                       hipStream_t stream);
 
+/* Kernels the library launches, as counted by gsq_timing_read. */
+enum {
+  GSQ_KERNEL_INIT = 0,      /* H symmetrisation, scale and logit initialisation        */
+  GSQ_KERNEL_FORWARD = 1,   /* the sample of Alg. 1 and the residual R                 */
+  GSQ_KERNEL_CONTRACT = 2,  /* P = R H, G = -2 P, loss partials                         */
+  GSQ_KERNEL_REDUCE = 3,    /* loss partials -> loss                                    */
+  GSQ_KERNEL_BACKWARD = 4,  /* gradient + Adam (+ the next step's sample)               */
+  GSQ_KERNEL_HARDEN = 5,    /* argmax, effective scales, hard residual                  */
+  GSQ_KERNEL_PACK = 6,      /* bitstream / super-block packing                          */
+  GSQ_NUM_KERNELS = 7
+};
+
+/*
+ * Kernel timing.  gsq_timing(h, 1) makes every later call record a HIP event pair
+ * around each kernel it enqueues (on the caller's stream); gsq_timing(h, 0) stops.
+ * gsq_timing_read synchronises `stream`, adds the elapsed time (ms) and the launch
+ * count of each kernel kind since the last reset into ms[GSQ_NUM_KERNELS] and
+ * launches[GSQ_NUM_KERNELS] (host arrays, either may be NULL), and clears them if
+ * reset != 0.
+ */
+gsq_status gsq_timing(gsq_layer* h, int32_t enable);
+gsq_status gsq_timing_read(gsq_layer* h, double* ms, int64_t* launches, int32_t reset,
+                           hipStream_t stream);
+
 /* Synchronise the stream and report the sticky non-finite flag (GSQ_OK or GSQ_ENONFINITE). */
 gsq_status gsq_check(gsq_layer* h, hipStream_t stream);
 

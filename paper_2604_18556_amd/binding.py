@@ -19,7 +19,8 @@ STATUS_NAMES = {0: "GSQ_OK", -1: "GSQ_EINVAL", -2: "GSQ_ENOMEM", -3: "GSQ_EHIP",
 
 EXPORTS = ("gsq_layer_init", "gsq_step", "gsq_harden", "gsq_packed_size", "gsq_pack",
            "gsq_get_state", "gsq_set_state", "gsq_get_intermediates", "gsq_gumbel", "gsq_check",
-           "gsq_layer_destroy", "gsq_last_error")
+           "gsq_layer_destroy", "gsq_last_error", "gsq_timing", "gsq_timing_read")
+KERNEL_NAMES = ("init", "forward", "contract", "reduce", "backward", "harden", "pack")
 
 
 class GsqError(RuntimeError):
@@ -120,9 +121,11 @@ def load(path=None):
     lib.gsq_check.argtypes = [vp, vp]
     lib.gsq_layer_destroy.argtypes = [vp]
     lib.gsq_last_error.restype = ctypes.c_char_p
+    lib.gsq_timing.argtypes = [vp, i32]
+    lib.gsq_timing_read.argtypes = [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64), i32, vp]
     for name in ("gsq_layer_init", "gsq_step", "gsq_harden", "gsq_pack", "gsq_get_state",
                  "gsq_set_state", "gsq_get_intermediates", "gsq_gumbel", "gsq_check",
-                 "gsq_layer_destroy"):
+                 "gsq_layer_destroy", "gsq_timing", "gsq_timing_read"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -206,6 +209,17 @@ class Layer:
 
     def intermediates(self, residual=None, grad=None, stream=None):
         _check(load().gsq_get_intermediates(self.handle, _ptr(residual), _ptr(grad), _stream(stream)))
+
+    def timing(self, enable):
+        _check(load().gsq_timing(self.handle, 1 if enable else 0))
+
+    def timing_read(self, reset=True, stream=None):
+        """{kernel: (total ms, launches)} since the last reset (synchronises the stream)."""
+        n = len(KERNEL_NAMES)
+        ms = (ctypes.c_double * n)()
+        cnt = (ctypes.c_int64 * n)()
+        _check(load().gsq_timing_read(self.handle, ms, cnt, 1 if reset else 0, _stream(stream)))
+        return {KERNEL_NAMES[k]: (ms[k], cnt[k]) for k in range(n)}
 
     def check(self, stream=None):
         _check(load().gsq_check(self.handle, _stream(stream)))

@@ -74,6 +74,11 @@ gsq_status validate_config(const gsq_config* c) {
 
 void free_layer(gsq::Layer* L) {
   if (!L) return;
+  for (auto& p : L->pending) {
+    (void)hipEventDestroy(p.second.first);
+    (void)hipEventDestroy(p.second.second);
+  }
+  for (hipEvent_t e : L->event_pool) (void)hipEventDestroy(e);
   void* bufs[] = {L->W, L->H, L->L, L->M, L->V, L->S, L->MS, L->VS, L->R[0], L->R[1],
                   L->G, L->partials, L->flag, L->sb_d, L->sb_sc, L->codes};
   for (void* p : bufs)
@@ -90,6 +95,51 @@ bool alloc(T** p, size_t bytes) {
   }
   *p = static_cast<T*>(q);
   return true;
+}
+
+// Event pair around one launch when timing is on (gsq_timing).
+constexpr size_t kMaxPending = 8192;
+
+hipError_t harvest(gsq::Layer& L) {
+  for (auto& p : L.pending) {
+    hipError_t e = hipEventSynchronize(p.second.second);
+    if (e != hipSuccess) return e;
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, p.second.first, p.second.second);
+    if (e != hipSuccess) return e;
+    L.timed_ms[p.first] += ms;
+    L.timed_launches[p.first] += 1;
+    L.event_pool.push_back(p.second.first);
+    L.event_pool.push_back(p.second.second);
+  }
+  L.pending.clear();
+  return hipSuccess;
+}
+
+hipError_t take_event(gsq::Layer& L, hipEvent_t* e) {
+  if (!L.event_pool.empty()) {
+    *e = L.event_pool.back();
+    L.event_pool.pop_back();
+    return hipSuccess;
+  }
+  return hipEventCreate(e);
+}
+
+template <class F>
+hipError_t timed(gsq::Layer& L, int kind, hipStream_t s, F&& launch) {
+  if (!L.timing) return launch();
+  if (L.pending.size() >= kMaxPending) {
+    hipError_t e = harvest(L);
+    if (e != hipSuccess) return e;
+  }
+  hipEvent_t e0, e1;
+  hipError_t e = take_event(L, &e0);
+  if (e == hipSuccess) e = take_event(L, &e1);
+  if (e == hipSuccess) e = hipEventRecord(e0, s);
+  if (e == hipSuccess) e = launch();
+  if (e == hipSuccess) e = hipEventRecord(e1, s);
+  if (e == hipSuccess) L.pending.push_back({kind, {e0, e1}});
+  return e;
 }
 
 gsq_status check_flag(gsq::Layer* h, hipStream_t s) {
@@ -158,7 +208,7 @@ gsq_status gsq_layer_init(const gsq_config* cfg, const void* W, int32_t w_dtype,
   }
   auto run = [&]() -> gsq_status {
     GSQ_HIP(hipMemcpyAsync(L.W, W, L.N * (L.w_bf16 ? 2 : 4), hipMemcpyDeviceToDevice, stream));
-    GSQ_HIP(gsq::launch_symmetrize_h(H, L.H, L.B, L.I, L.Ipad, L.bf16, stream));
+    GSQ_HIP(timed(L, GSQ_KERNEL_INIT, stream, [&] { return gsq::launch_symmetrize_h(H, L.H, L.B, L.I, L.Ipad, L.bf16, stream); }));
     GSQ_HIP(hipMemsetAsync(L.R[0], 0, npad * relem, stream));   // padding stays zero
     GSQ_HIP(hipMemsetAsync(L.R[1], 0, npad * relem, stream));
     GSQ_HIP(hipMemsetAsync(L.M, 0, L.K * L.N * 4, stream));
@@ -168,11 +218,11 @@ gsq_status gsq_layer_init(const gsq_config* cfg, const void* W, int32_t w_dtype,
     GSQ_HIP(hipMemsetAsync(L.flag, 0, sizeof(int), stream));
     float cmax = 0.f;
     for (int k = 0; k < L.K; ++k) cmax = std::fmax(cmax, std::fabs(cfg->levels[k]));
-    GSQ_HIP(gsq::launch_init_scales(L, scales_init, cmax, stream));
+    GSQ_HIP(timed(L, GSQ_KERNEL_INIT, stream, [&] { return gsq::launch_init_scales(L, scales_init, cmax, stream); }));
     double mids[8] = {0};
     for (int k = 0; k + 1 < L.K; ++k)
       mids[k] = 0.5 * ((double)cfg->levels[k] + (double)cfg->levels[k + 1]);
-    GSQ_HIP(gsq::launch_init_logits(L, mids, stream));
+    GSQ_HIP(timed(L, GSQ_KERNEL_INIT, stream, [&] { return gsq::launch_init_logits(L, mids, stream); }));
     return GSQ_OK;
   };
   st = run();
@@ -220,11 +270,11 @@ gsq_status gsq_step(gsq_layer* h, const gsq_step_params* p, float* loss_out, hip
                     L.r_noise == a.noise;
   if (!have) {
     a.Rout = L.R[L.cur];
-    GSQ_HIP(gsq::launch_forward(L, a, stream));
+    GSQ_HIP(timed(L, GSQ_KERNEL_FORWARD, stream, [&] { return gsq::launch_forward(L, a, stream); }));
   }
   const int use = L.cur;
-  GSQ_HIP(gsq::launch_contract(L, L.R[use], loss_out != nullptr, stream));
-  if (loss_out) GSQ_HIP(gsq::launch_reduce_loss(L, loss_out, stream));
+  GSQ_HIP(timed(L, GSQ_KERNEL_CONTRACT, stream, [&] { return gsq::launch_contract(L, L.R[use], loss_out != nullptr, stream); }));
+  if (loss_out) GSQ_HIP(timed(L, GSQ_KERNEL_REDUCE, stream, [&] { return gsq::launch_reduce_loss(L, loss_out, stream); }));
 
   const double n = (double)(L.t + 1);
   const double bc1 = 1.0 - std::pow((double)p->beta1, n);
@@ -244,7 +294,7 @@ gsq_status gsq_step(gsq_layer* h, const gsq_step_params* p, float* loss_out, hip
   a.inv_tau_n = a.fuse ? 1.0f / p->tau_next : 0.f;
   a.inv_tau_n_d = a.fuse ? 1.0 / (double)p->tau_next : 0.0;
   a.Rout = L.R[1 - use];
-  GSQ_HIP(gsq::launch_backward(L, a, p->lr_scales > 0.f, stream));
+  GSQ_HIP(timed(L, GSQ_KERNEL_BACKWARD, stream, [&] { return gsq::launch_backward(L, a, p->lr_scales > 0.f, stream); }));
 
   L.last = use;
   L.t += 1;
@@ -274,11 +324,11 @@ gsq_status gsq_harden(gsq_layer* h, uint8_t* codes, float* scales, float* hard_l
     Rh = L.R[buf];
     L.r_valid = false;
   }
-  GSQ_HIP(gsq::launch_harden(L, codes ? codes : L.codes, Rh, stream));
-  GSQ_HIP(gsq::launch_eff_scales(L, scales, stream));
+  GSQ_HIP(timed(L, GSQ_KERNEL_HARDEN, stream, [&] { return gsq::launch_harden(L, codes ? codes : L.codes, Rh, stream); }));
+  GSQ_HIP(timed(L, GSQ_KERNEL_HARDEN, stream, [&] { return gsq::launch_eff_scales(L, scales, stream); }));
   if (hard_loss_out) {
-    GSQ_HIP(gsq::launch_contract(L, Rh, true, stream));
-    GSQ_HIP(gsq::launch_reduce_loss(L, hard_loss_out, stream));
+    GSQ_HIP(timed(L, GSQ_KERNEL_CONTRACT, stream, [&] { return gsq::launch_contract(L, Rh, true, stream); }));
+    GSQ_HIP(timed(L, GSQ_KERNEL_REDUCE, stream, [&] { return gsq::launch_reduce_loss(L, hard_loss_out, stream); }));
     L.last = -1;   // G now belongs to the hard residual
   }
   return check_flag(h, stream);
@@ -292,8 +342,8 @@ gsq_status gsq_pack(gsq_layer* h, void* packed, size_t packed_bytes, hipStream_t
   if (packed_bytes < need)
     return fail(GSQ_EINVAL, "packed buffer has %zu bytes, needs %zu", packed_bytes, need);
   gsq::Layer& L = *h;
-  GSQ_HIP(gsq::launch_harden(L, L.codes, nullptr, stream));
-  GSQ_HIP(gsq::launch_pack(L, L.codes, static_cast<uint8_t*>(packed), stream));
+  GSQ_HIP(timed(L, GSQ_KERNEL_HARDEN, stream, [&] { return gsq::launch_harden(L, L.codes, nullptr, stream); }));
+  GSQ_HIP(timed(L, GSQ_KERNEL_PACK, stream, [&] { return gsq::launch_pack(L, L.codes, static_cast<uint8_t*>(packed), stream); }));
   return check_flag(h, stream);
 }
 
@@ -355,6 +405,30 @@ gsq_status gsq_gumbel(const gsq_config* cfg, int64_t e0, int64_t count, int64_t 
   if (count == 0) return GSQ_OK;
   if (!g_out) return fail(GSQ_EINVAL, "g_out is NULL");
   GSQ_HIP(gsq::launch_gumbel(*cfg, e0, count, t, g_out, stream));
+  return GSQ_OK;
+}
+
+gsq_status gsq_timing(gsq_layer* h, int32_t enable) {
+  g_err.clear();
+  if (!h) return fail(GSQ_EINVAL, "handle is NULL");
+  h->timing = enable != 0;
+  return GSQ_OK;
+}
+
+gsq_status gsq_timing_read(gsq_layer* h, double* ms, int64_t* launches, int32_t reset,
+                           hipStream_t stream) {
+  g_err.clear();
+  if (!h) return fail(GSQ_EINVAL, "handle is NULL");
+  GSQ_HIP(hipStreamSynchronize(stream));
+  GSQ_HIP(harvest(*h));
+  for (int k = 0; k < GSQ_NUM_KERNELS; ++k) {
+    if (ms) ms[k] = h->timed_ms[k];
+    if (launches) launches[k] = h->timed_launches[k];
+    if (reset) {
+      h->timed_ms[k] = 0.0;
+      h->timed_launches[k] = 0;
+    }
+  }
   return GSQ_OK;
 }
 

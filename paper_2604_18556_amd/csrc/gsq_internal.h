@@ -3,6 +3,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <utility>
+#include <vector>
+
 #include "gsq.h"
 
 namespace gsq {
@@ -63,6 +66,12 @@ struct Layer {
   float r_tau = 0.f, r_kappa = 0.f;
   int r_noise = 0;
   int last = -1;          // R buffer of the most recent step (-1: none)
+  // kernel timing (gsq_timing)
+  bool timing = false;
+  std::vector<hipEvent_t> event_pool;
+  std::vector<std::pair<int, std::pair<hipEvent_t, hipEvent_t>>> pending;
+  double timed_ms[GSQ_NUM_KERNELS] = {0};
+  int64_t timed_launches[GSQ_NUM_KERNELS] = {0};
 };
 
 // ---- launchers (gsq_elem.hip)
