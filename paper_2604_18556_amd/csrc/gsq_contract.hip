@@ -17,8 +17,11 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int BM = kTileM, BN = kTileN, BK = 32;
-constexpr int LDS_STRIDE = BK + 8;   // bf16 per LDS row; 16 bytes of padding against bank conflicts
+constexpr int BM = kTileM, BN = kTileN, BK = 64;
+constexpr int ROW_BYTES = BK * 2;                        // one 64-wide bf16 row of a slab
+constexpr int SLAB_BYTES = BM * ROW_BYTES;               // 32 KB per operand per stage
+constexpr size_t LDS_BYTES = 2 * 2 * SLAB_BYTES;         // two operands, two stages
+constexpr int GROUP_M = 8;           // tile rows swept together for L2 reuse
 
 __device__ __forceinline__ void block_sum_to(double x, double* out) {
   __shared__ double red[256];
@@ -31,74 +34,100 @@ __device__ __forceinline__ void block_sum_to(double x, double* out) {
   if (threadIdx.x == 0) *out = red[0];
 }
 
-// One 128 x 128 tile of G per workgroup; four wavefronts each own 64 x 64 as 2 x 2 MFMA tiles.
-__global__ __launch_bounds__(256) void k_contract_bf16(const uint16_t* __restrict__ R,
-                                                       const uint16_t* __restrict__ H,
-                                                       float* __restrict__ G,
-                                                       double* __restrict__ partials, int64_t Opad,
-                                                       int64_t Ipad, int want_loss) {
-  __shared__ __attribute__((aligned(16))) uint16_t As[BM * LDS_STRIDE];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[BN * LDS_STRIDE];
+// Tile of block `bid`.  Workgroups are handed to the 8 XCDs round-robin; renumbering so
+// each XCD owns a contiguous range, then sweeping GROUP_M tile rows at a time, keeps the
+// R and H panels a group shares in the same XCD's L2.
+__device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
+  const int nblk = tiles_m * tiles_n;
+  int lin = bid;
+  if ((nblk & 7) == 0) lin = (bid & 7) * (nblk >> 3) + (bid >> 3);
+  const int per_group = GROUP_M * tiles_n;
+  const int first_m = (lin / per_group) * GROUP_M;
+  const int gsz = min(tiles_m - first_m, GROUP_M);
+  const int r = lin % per_group;
+  tm = first_m + r % gsz;
+  tn = r / gsz;
+}
+
+// One 256 x 256 tile of G per workgroup; four wavefronts each own 128 x 128 as 4 x 4 MFMA
+// 32x32x16 tiles.  The K loop is double-buffered in LDS and fed by direct global->LDS loads
+// (16 bytes per lane, no staging registers): while the matrix cores consume one 64-wide slab
+// of R and H, the next slab streams into the other buffer.
+//
+// LDS layout of a slab: row r occupies 128 bytes as eight 16-byte chunks, chunk c of the row
+// stored at position c ^ (r & 7).  A fragment read (eight consecutive rows, one chunk each)
+// then touches eight different bank groups.
+__device__ __forceinline__ void load_slab(const uint16_t* src, int64_t ld, int64_t k0,
+                                          uint8_t* lds, int wave, int lane) {
+  // wave w fills rows 64 w .. 64 w + 63, eight rows (1 KB of LDS) per instruction
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int row = wave * 64 + j * 8 + (lane >> 3);
+    const int chunk = (lane & 7) ^ (row & 7);
+    const uint16_t* g = src + row * ld + k0 + chunk * 8;
+    __builtin_amdgcn_global_load_lds(g, lds + (wave * 64 + j * 8) * ROW_BYTES, 16, 0, 0);
+  }
+}
+
+__device__ __forceinline__ bf16x8 read_frag(const uint8_t* lds, int row, int chunk) {
+  return *reinterpret_cast<const bf16x8*>(lds + row * ROW_BYTES + ((chunk ^ (row & 7)) << 4));
+}
+
+__global__ __launch_bounds__(256, 1) void k_contract_bf16(const uint16_t* __restrict__ R,
+                                                          const uint16_t* __restrict__ H,
+                                                          float* __restrict__ G,
+                                                          double* __restrict__ partials,
+                                                          int64_t Opad, int64_t Ipad, int tiles_m,
+                                                          int tiles_n, int want_loss) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const int64_t b = blockIdx.z;
-  const int64_t m0 = (int64_t)blockIdx.y * BM, n0 = (int64_t)blockIdx.x * BN;
+  int tm, tn;
+  tile_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
+  const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
   const uint16_t* A = R + b * Opad * Ipad + m0 * Ipad;
   const uint16_t* Bt = H + b * Ipad * Ipad + n0 * Ipad;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
 
-  f32x16 acc[2][2];
+  f32x16 acc[4][4];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // 128 rows x 32 bf16 per operand tile = 512 chunks of 16 bytes, two per thread
-  uint4 ra[2], rb[2];
-  auto gload = [&](int64_t k0) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int c = tid + 256 * i, row = c >> 2, col = (c & 3) * 8;
-      ra[i] = *reinterpret_cast<const uint4*>(A + row * Ipad + k0 + col);
-      rb[i] = *reinterpret_cast<const uint4*>(Bt + row * Ipad + k0 + col);
-    }
-  };
-  auto lstore = [&]() {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int c = tid + 256 * i, row = c >> 2, col = (c & 3) * 8;
-      *reinterpret_cast<uint4*>(As + row * LDS_STRIDE + col) = ra[i];
-      *reinterpret_cast<uint4*>(Bs + row * LDS_STRIDE + col) = rb[i];
-    }
-  };
-
   const int64_t nk = Ipad / BK;
-  gload(0);
-  lstore();
+  load_slab(A, Ipad, 0, smem, wave, lane);
+  load_slab(Bt, Ipad, 0, smem + SLAB_BYTES, wave, lane);
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   for (int64_t kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) gload((kt + 1) * BK);
+    const int stage = (int)(kt & 1);
+    if (kt + 1 < nk) {
+      uint8_t* nxt = smem + (stage ^ 1) * 2 * SLAB_BYTES;
+      load_slab(A, Ipad, (kt + 1) * BK, nxt, wave, lane);
+      load_slab(Bt, Ipad, (kt + 1) * BK, nxt + SLAB_BYTES, wave, lane);
+    }
+    const uint8_t* As = smem + stage * 2 * SLAB_BYTES;
+    const uint8_t* Bs = As + SLAB_BYTES;
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
-      bf16x8 af[2], bv[2];
-      const int col = ks * 16 + (lane >> 5) * 8;
+      bf16x8 af[4], bv[4];
+      const int chunk = ks * 2 + (lane >> 5);
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        af[i] = *reinterpret_cast<const bf16x8*>(As + (wm * 64 + i * 32 + (lane & 31)) * LDS_STRIDE + col);
-        bv[i] = *reinterpret_cast<const bf16x8*>(Bs + (wn * 64 + i * 32 + (lane & 31)) * LDS_STRIDE + col);
+      for (int i = 0; i < 4; ++i) {
+        af[i] = read_frag(As, wm * 128 + i * 32 + (lane & 31), chunk);
+        bv[i] = read_frag(Bs, wn * 128 + i * 32 + (lane & 31), chunk);
       }
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < 4; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bv[j], acc[i][j], 0, 0, 0);
     }
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if (kt + 1 < nk) {
-      lstore();
-      __syncthreads();
-    }
   }
 
   // 32 x 32 accumulator layout: lane l, register r -> row 8*(r/4) + 4*(l/32) + r%4, column l%32
@@ -106,19 +135,18 @@ __global__ __launch_bounds__(256) void k_contract_bf16(const uint16_t* __restric
   const uint16_t* Rb = R + b * Opad * Ipad;
   double lsum = 0.0;
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int64_t row = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        const int64_t col = n0 + wn * 64 + j * 32 + (lane & 31);
+        const int64_t row = m0 + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        const int64_t col = n0 + wn * 128 + j * 32 + (lane & 31);
         const float p = acc[i][j][r];
         Gb[row * Ipad + col] = -2.f * p;
         if (want_loss) lsum += (double)bf16_to_f32(Rb[row * Ipad + col]) * (double)p;
       }
-  if (want_loss)
-    block_sum_to(lsum, partials + (b * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x);
+  if (want_loss) block_sum_to(lsum, partials + b * (int64_t)tiles_m * tiles_n + tm * tiles_n + tn);
 }
 
 // FP32 precision: 64 x 64 tile per workgroup, 4 x 4 outputs per thread, fp64 accumulation.
@@ -203,10 +231,18 @@ int64_t contract_tiles_per_batch(const Layer& L) {
 
 hipError_t launch_contract(const Layer& L, const void* R, bool want_loss, hipStream_t s) {
   if (L.bf16) {
-    dim3 grid((unsigned)(L.Ipad / BN), (unsigned)(L.Opad / BM), (unsigned)L.B);
-    hipLaunchKernelGGL(k_contract_bf16, grid, dim3(256), 0, s, static_cast<const uint16_t*>(R),
-                       static_cast<const uint16_t*>(L.H), L.G, L.partials, L.Opad, L.Ipad,
-                       want_loss ? 1 : 0);
+    static bool attr_set = false;
+    if (!attr_set) {
+      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k_contract_bf16),
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)LDS_BYTES);
+      if (e != hipSuccess) return e;
+      attr_set = true;
+    }
+    const int tiles_m = (int)(L.Opad / BM), tiles_n = (int)(L.Ipad / BN);
+    dim3 grid((unsigned)(tiles_m * tiles_n), 1, (unsigned)L.B);
+    hipLaunchKernelGGL(k_contract_bf16, grid, dim3(256), LDS_BYTES, s,
+                       static_cast<const uint16_t*>(R), static_cast<const uint16_t*>(L.H), L.G,
+                       L.partials, L.Opad, L.Ipad, tiles_m, tiles_n, want_loss ? 1 : 0);
   } else {
     dim3 grid((unsigned)(L.Ipad / TN), (unsigned)(L.Opad / TM), (unsigned)L.B);
     hipLaunchKernelGGL(k_contract_f32, grid, dim3(256), 0, s, static_cast<const float*>(R),

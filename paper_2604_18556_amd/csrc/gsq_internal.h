@@ -10,9 +10,9 @@
 
 namespace gsq {
 
-constexpr int kTileM = 128;   // contraction tile (rows of R / G)
-constexpr int kTileN = 128;   // contraction tile (columns of G = rows of H)
-constexpr int kPadK = 128;    // padding of the inner dimension (H is padded with zeros)
+constexpr int kTileM = 256;   // contraction tile (rows of R / G)
+constexpr int kTileN = 256;   // contraction tile (columns of G = rows of H)
+constexpr int kPadK = 256;    // padding of the inner dimension (H is padded with zeros)
 
 // Everything an elementwise kernel needs, passed by value.
 struct ElemArgs {
