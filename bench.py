@@ -108,10 +108,17 @@ def copy_calibration(dev, gib=1):
     n = gib * (1 << 30) // 4
     src = torch.ones(n, dtype=torch.float32, device=dev)
     dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
     for _ in range(5):
         dst.copy_(src)
+    end.record()
     torch.cuda.synchronize()
-    print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 5}))
+    ms = start.elapsed_time(end) / 5
+    print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 6,
+                      "ms_per_copy": ms, "copy_GBs": 2 * n * 4 / (ms * 1e-3) / 1e9}))
 
 
 def main():

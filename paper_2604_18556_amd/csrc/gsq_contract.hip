@@ -17,10 +17,12 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int BM = kTileM, BN = kTileN, BK = 64;
-constexpr int ROW_BYTES = BK * 2;                        // one 64-wide bf16 row of a slab
-constexpr int SLAB_BYTES = BM * ROW_BYTES;               // 32 KB per operand per stage
-constexpr size_t LDS_BYTES = 2 * 2 * SLAB_BYTES;         // two operands, two stages
+constexpr int BM = kTileM, BN = kTileN, BK = 32;
+constexpr int STAGES = 4;                                // LDS ring of K slabs
+constexpr int ROW_BYTES = BK * 2;                        // one 32-wide bf16 row of a slab
+constexpr int SLAB_BYTES = BM * ROW_BYTES;               // 16 KB per operand per stage
+constexpr size_t LDS_BYTES = (size_t)STAGES * 2 * SLAB_BYTES;
+constexpr int LOADS_PER_STAGE = 2 * SLAB_BYTES / 1024 / 4;   // 1 KB loads per wavefront per stage
 constexpr int GROUP_M = 8;           // tile rows swept together for L2 reuse
 
 __device__ __forceinline__ void block_sum_to(double x, double* out) {
@@ -50,27 +52,45 @@ __device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& 
 }
 
 // One 256 x 256 tile of G per workgroup; four wavefronts each own 128 x 128 as 4 x 4 MFMA
-// 32x32x16 tiles.  The K loop is double-buffered in LDS and fed by direct global->LDS loads
-// (16 bytes per lane, no staging registers): while the matrix cores consume one 64-wide slab
-// of R and H, the next slab streams into the other buffer.
+// 32x32x16 tiles.  K slabs 32 wide stream through a ring of four LDS buffers by direct
+// global->LDS loads (16 bytes per lane, no staging registers): while the matrix cores consume
+// slab k, slabs k+1..k+3 are in flight.
 //
-// LDS layout of a slab: row r occupies 128 bytes as eight 16-byte chunks, chunk c of the row
-// stored at position c ^ (r & 7).  A fragment read (eight consecutive rows, one chunk each)
-// then touches eight different bank groups.
+// LDS layout of a slab: row r occupies 64 bytes as four 16-byte chunks, chunk c stored at
+// position c ^ f(r), f(r) = ((r >> 1) ^ (r >> 3)) & 3.  The fragment reads (consecutive rows,
+// one chunk each) then fall on distinct banks for 8- and 16-lane access phases and for 32 or
+// 64 banks.
+__device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
+
 __device__ __forceinline__ void load_slab(const uint16_t* src, int64_t ld, int64_t k0,
                                           uint8_t* lds, int wave, int lane) {
-  // wave w fills rows 64 w .. 64 w + 63, eight rows (1 KB of LDS) per instruction
+  // wave w fills rows 64 w .. 64 w + 63, sixteen rows (1 KB of LDS) per instruction
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int row = wave * 64 + j * 8 + (lane >> 3);
-    const int chunk = (lane & 7) ^ (row & 7);
+  for (int j = 0; j < 4; ++j) {
+    const int row = wave * 64 + j * 16 + (lane >> 2);
+    const int chunk = (lane & 3) ^ swz(row);
     const uint16_t* g = src + row * ld + k0 + chunk * 8;
-    __builtin_amdgcn_global_load_lds(g, lds + (wave * 64 + j * 8) * ROW_BYTES, 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(g, lds + (wave * 64 + j * 16) * ROW_BYTES, 16, 0, 0);
   }
 }
 
 __device__ __forceinline__ bf16x8 read_frag(const uint8_t* lds, int row, int chunk) {
-  return *reinterpret_cast<const bf16x8*>(lds + row * ROW_BYTES + ((chunk ^ (row & 7)) << 4));
+  return *reinterpret_cast<const bf16x8*>(lds + row * ROW_BYTES + ((chunk ^ swz(row)) << 4));
+}
+
+// Wait until at most n of this wavefront's vector-memory loads are outstanding (loads complete
+// in issue order), leaving LDS and scalar counters alone.
+template <int n>
+__device__ __forceinline__ void wait_vm() {
+  __builtin_amdgcn_s_waitcnt((n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14));
+}
+
+// Workgroup barrier for the slab ring.  The wavefront's own global->LDS loads have been
+// waited for (wait_vm) and its LDS reads are drained here; a plain s_barrier then suffices.
+// (__syncthreads would also drain every in-flight slab of the ring.)  The memory clobber
+// keeps the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void slab_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
 __global__ __launch_bounds__(256, 1) void k_contract_bf16(const uint16_t* __restrict__ R,
@@ -97,38 +117,65 @@ __global__ __launch_bounds__(256, 1) void k_contract_bf16(const uint16_t* __rest
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  const int64_t nk = Ipad / BK;
-  load_slab(A, Ipad, 0, smem, wave, lane);
-  load_slab(Bt, Ipad, 0, smem + SLAB_BYTES, wave, lane);
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  for (int64_t kt = 0; kt < nk; ++kt) {
-    const int stage = (int)(kt & 1);
-    if (kt + 1 < nk) {
-      uint8_t* nxt = smem + (stage ^ 1) * 2 * SLAB_BYTES;
-      load_slab(A, Ipad, (kt + 1) * BK, nxt, wave, lane);
-      load_slab(Bt, Ipad, (kt + 1) * BK, nxt + SLAB_BYTES, wave, lane);
-    }
-    const uint8_t* As = smem + stage * 2 * SLAB_BYTES;
-    const uint8_t* Bs = As + SLAB_BYTES;
+  const int64_t nk = Ipad / BK;   // a multiple of 8 (Ipad is a multiple of 256)
+  auto issue = [&](int64_t k) {
+    uint8_t* st = smem + (k % STAGES) * 2 * SLAB_BYTES;
+    load_slab(A, Ipad, k * BK, st, wave, lane);
+    load_slab(Bt, Ipad, k * BK, st + SLAB_BYTES, wave, lane);
+  };
+  const int frow_a = wm * 128 + (lane & 31), frow_b = wn * 128 + (lane & 31);
+  const int fchunk = lane >> 5;
+
+// fragments of slab K into register set S (A rows / B columns, two 16-deep halves)
+#define GSQ_READ(S, K)                                                                   \
+  do {                                                                                   \
+    const uint8_t* As_ = smem + ((K) % STAGES) * 2 * SLAB_BYTES;                         \
+    const uint8_t* Bs_ = As_ + SLAB_BYTES;                                               \
+    _Pragma("unroll") for (int h = 0; h < 2; ++h)                                        \
+      _Pragma("unroll") for (int i = 0; i < 4; ++i) {                                    \
+        S##a[h][i] = read_frag(As_, frow_a + i * 32, h * 2 + fchunk);                    \
+        S##b[h][i] = read_frag(Bs_, frow_b + i * 32, h * 2 + fchunk);                    \
+      }                                                                                  \
+  } while (0)
+#define GSQ_MFMA(S, H)                                                                   \
+  _Pragma("unroll") for (int i = 0; i < 4; ++i)                                          \
+    _Pragma("unroll") for (int j = 0; j < 4; ++j)                                        \
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(S##a[H][i], S##b[H][j], acc[i][j], 0, 0, 0)
+// One slab K held in set CUR: the first half of its MFMAs; then, once slab K+1 has landed and
+// every wavefront's reads of slab K have returned (barrier), refill slab K's slot with slab
+// K+STAGES and read slab K+1 into set NXT while the second half of slab K's MFMAs runs.
+#define GSQ_STEP(CUR, NXT, K)                                                            \
+  do {                                                                                   \
+    GSQ_MFMA(CUR, 0);                                                                    \
+    if ((K) + 1 < nk) {                                                                  \
+      const int64_t later_ = min((K) + STAGES - 1, nk - 1) - ((K) + 1);                  \
+      if (later_ >= 2) wait_vm<2 * LOADS_PER_STAGE>();                                   \
+      else if (later_ == 1) wait_vm<LOADS_PER_STAGE>();                                  \
+      else wait_vm<0>();                                                                 \
+      slab_barrier();                                                                    \
+      if ((K) + STAGES < nk) issue((K) + STAGES);                                        \
+      GSQ_READ(NXT, (K) + 1);                                                            \
+    }                                                                                    \
+    GSQ_MFMA(CUR, 1);                                                                    \
+    _Pragma("unroll") for (int q = 0; q < 16; ++q) {                                     \
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                                 \
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                 \
+    }                                                                                    \
+  } while (0)
+
+  bf16x8 f0a[2][4], f0b[2][4], f1a[2][4], f1b[2][4];
 #pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      bf16x8 af[4], bv[4];
-      const int chunk = ks * 2 + (lane >> 5);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        af[i] = read_frag(As, wm * 128 + i * 32 + (lane & 31), chunk);
-        bv[i] = read_frag(Bs, wn * 128 + i * 32 + (lane & 31), chunk);
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bv[j], acc[i][j], 0, 0, 0);
-    }
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
+  for (int k = 0; k < STAGES; ++k) issue(k);
+  wait_vm<(STAGES - 1) * LOADS_PER_STAGE>();
+  slab_barrier();
+  GSQ_READ(f0, 0);
+  for (int64_t kt = 0; kt < nk; kt += 2) {
+    GSQ_STEP(f0, f1, kt);
+    GSQ_STEP(f1, f0, kt + 1);
   }
+#undef GSQ_STEP
+#undef GSQ_MFMA
+#undef GSQ_READ
 
   // 32 x 32 accumulator layout: lane l, register r -> row 8*(r/4) + 4*(l/32) + r%4, column l%32
   float* Gb = G + b * Opad * Ipad;
