@@ -17,10 +17,10 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int BM = kTileM, BN = kTileN, BK = 32;
-constexpr int STAGES = 4;                                // LDS ring of K slabs
-constexpr int ROW_BYTES = BK * 2;                        // one 32-wide bf16 row of a slab
-constexpr int SLAB_BYTES = BM * ROW_BYTES;               // 16 KB per operand per stage
+constexpr int BM = kTileM, BN = kTileN, BK = 64;
+constexpr int STAGES = 2;                                // LDS ring of K slabs
+constexpr int ROW_BYTES = BK * 2;                        // one 64-wide bf16 row: a full cache line
+constexpr int SLAB_BYTES = BM * ROW_BYTES;               // 32 KB per operand per stage
 constexpr size_t LDS_BYTES = (size_t)STAGES * 2 * SLAB_BYTES;
 constexpr int LOADS_PER_STAGE = 2 * SLAB_BYTES / 1024 / 4;   // 1 KB loads per wavefront per stage
 constexpr int GROUP_M = 8;           // tile rows swept together for L2 reuse
@@ -52,25 +52,24 @@ __device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& 
 }
 
 // One 256 x 256 tile of G per workgroup; four wavefronts each own 128 x 128 as 4 x 4 MFMA
-// 32x32x16 tiles.  K slabs 32 wide stream through a ring of four LDS buffers by direct
-// global->LDS loads (16 bytes per lane, no staging registers): while the matrix cores consume
-// slab k, slabs k+1..k+3 are in flight.
+// 32x32x16 tiles.  K slabs 64 wide (whole 128-byte lines of R and H) stream through two LDS
+// buffers by direct global->LDS loads (16 bytes per lane, no staging registers).
 //
-// LDS layout of a slab: row r occupies 64 bytes as four 16-byte chunks, chunk c stored at
-// position c ^ f(r), f(r) = ((r >> 1) ^ (r >> 3)) & 3.  The fragment reads (consecutive rows,
-// one chunk each) then fall on distinct banks for 8- and 16-lane access phases and for 32 or
-// 64 banks.
-__device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
+// LDS layout of a slab: row r occupies 128 bytes as eight 16-byte chunks, chunk c stored at
+// position c ^ f(r), f(r) = (r ^ (r >> 3)) & 7.  The fragment reads (consecutive rows, one
+// chunk each) then fall on distinct banks for 8- and 16-lane access phases and for 32 or 64
+// banks.
+__device__ __forceinline__ int swz(int r) { return (r ^ (r >> 3)) & 7; }
 
 __device__ __forceinline__ void load_slab(const uint16_t* src, int64_t ld, int64_t k0,
                                           uint8_t* lds, int wave, int lane) {
-  // wave w fills rows 64 w .. 64 w + 63, sixteen rows (1 KB of LDS) per instruction
+  // wave w fills rows 64 w .. 64 w + 63, eight rows (1 KB of LDS) per instruction
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int row = wave * 64 + j * 16 + (lane >> 2);
-    const int chunk = (lane & 3) ^ swz(row);
+  for (int j = 0; j < 8; ++j) {
+    const int row = wave * 64 + j * 8 + (lane >> 3);
+    const int chunk = (lane & 7) ^ swz(row);
     const uint16_t* g = src + row * ld + k0 + chunk * 8;
-    __builtin_amdgcn_global_load_lds(g, lds + (wave * 64 + j * 16) * ROW_BYTES, 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(g, lds + (wave * 64 + j * 8) * ROW_BYTES, 16, 0, 0);
   }
 }
 
@@ -117,7 +116,7 @@ __global__ __launch_bounds__(256, 1) void k_contract_bf16(const uint16_t* __rest
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  const int64_t nk = Ipad / BK;   // a multiple of 8 (Ipad is a multiple of 256)
+  const int64_t nk = Ipad / BK;   // a multiple of 4 (Ipad is a multiple of 256)
   auto issue = [&](int64_t k) {
     uint8_t* st = smem + (k % STAGES) * 2 * SLAB_BYTES;
     load_slab(A, Ipad, k * BK, st, wave, lane);
@@ -126,54 +125,45 @@ __global__ __launch_bounds__(256, 1) void k_contract_bf16(const uint16_t* __rest
   const int frow_a = wm * 128 + (lane & 31), frow_b = wn * 128 + (lane & 31);
   const int fchunk = lane >> 5;
 
-// fragments of slab K into register set S (A rows / B columns, two 16-deep halves)
-#define GSQ_READ(S, K)                                                                   \
+// fragments of sub-steps 2 HALF and 2 HALF + 1 of slab K into register set S
+#define GSQ_READ(S, K, HALF)                                                             \
   do {                                                                                   \
     const uint8_t* As_ = smem + ((K) % STAGES) * 2 * SLAB_BYTES;                         \
     const uint8_t* Bs_ = As_ + SLAB_BYTES;                                               \
     _Pragma("unroll") for (int h = 0; h < 2; ++h)                                        \
       _Pragma("unroll") for (int i = 0; i < 4; ++i) {                                    \
-        S##a[h][i] = read_frag(As_, frow_a + i * 32, h * 2 + fchunk);                    \
-        S##b[h][i] = read_frag(Bs_, frow_b + i * 32, h * 2 + fchunk);                    \
+        const int c_ = (2 * (HALF) + h) * 2 + fchunk;                                    \
+        S##a[h][i] = read_frag(As_, frow_a + i * 32, c_);                                \
+        S##b[h][i] = read_frag(Bs_, frow_b + i * 32, c_);                                \
       }                                                                                  \
   } while (0)
-#define GSQ_MFMA(S, H)                                                                   \
-  _Pragma("unroll") for (int i = 0; i < 4; ++i)                                          \
-    _Pragma("unroll") for (int j = 0; j < 4; ++j)                                        \
-      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(S##a[H][i], S##b[H][j], acc[i][j], 0, 0, 0)
-// One slab K held in set CUR: the first half of its MFMAs; then, once slab K+1 has landed and
-// every wavefront's reads of slab K have returned (barrier), refill slab K's slot with slab
-// K+STAGES and read slab K+1 into set NXT while the second half of slab K's MFMAs runs.
-#define GSQ_STEP(CUR, NXT, K)                                                            \
-  do {                                                                                   \
-    GSQ_MFMA(CUR, 0);                                                                    \
-    if ((K) + 1 < nk) {                                                                  \
-      const int64_t later_ = min((K) + STAGES - 1, nk - 1) - ((K) + 1);                  \
-      if (later_ >= 2) wait_vm<2 * LOADS_PER_STAGE>();                                   \
-      else if (later_ == 1) wait_vm<LOADS_PER_STAGE>();                                  \
-      else wait_vm<0>();                                                                 \
-      slab_barrier();                                                                    \
-      if ((K) + STAGES < nk) issue((K) + STAGES);                                        \
-      GSQ_READ(NXT, (K) + 1);                                                            \
-    }                                                                                    \
-    GSQ_MFMA(CUR, 1);                                                                    \
-    _Pragma("unroll") for (int q = 0; q < 16; ++q) {                                     \
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                                 \
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                 \
-    }                                                                                    \
-  } while (0)
+#define GSQ_MFMA(S)                                                                      \
+  _Pragma("unroll") for (int h = 0; h < 2; ++h)                                          \
+    _Pragma("unroll") for (int i = 0; i < 4; ++i)                                        \
+      _Pragma("unroll") for (int j = 0; j < 4; ++j)                                      \
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(S##a[h][i], S##b[h][j], acc[i][j], 0, 0, 0)
 
-  bf16x8 f0a[2][4], f0b[2][4], f1a[2][4], f1b[2][4];
-#pragma unroll
-  for (int k = 0; k < STAGES; ++k) issue(k);
-  wait_vm<(STAGES - 1) * LOADS_PER_STAGE>();
+  // p: first half (sub-steps 0, 1) of the current slab; q: second half (sub-steps 2, 3)
+  bf16x8 pa[2][4], pb[2][4], qa[2][4], qb[2][4];
+  issue(0);
+  issue(1);
+  wait_vm<LOADS_PER_STAGE>();
   slab_barrier();
-  GSQ_READ(f0, 0);
-  for (int64_t kt = 0; kt < nk; kt += 2) {
-    GSQ_STEP(f0, f1, kt);
-    GSQ_STEP(f1, f0, kt + 1);
+  GSQ_READ(p, 0, 0);
+  for (int64_t kt = 0; kt < nk; ++kt) {
+    // phase 1: read the second half of slab kt while its first half feeds the matrix cores
+    GSQ_READ(q, kt, 1);
+    GSQ_MFMA(p);
+    // phase 2: slab kt+1 (issued one slab ago) must have landed, and every wavefront's reads
+    // of slab kt must have returned before its buffer is refilled with slab kt+2
+    if (kt + 1 < nk) {
+      wait_vm<0>();
+      slab_barrier();
+      if (kt + 2 < nk) issue(kt + 2);
+      GSQ_READ(p, kt + 1, 0);
+    }
+    GSQ_MFMA(q);
   }
-#undef GSQ_STEP
 #undef GSQ_MFMA
 #undef GSQ_READ
 
