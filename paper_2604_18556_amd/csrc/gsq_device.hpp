@@ -31,9 +31,11 @@ __device__ __forceinline__ U4 noise_words(uint64_t seed, uint64_t e, uint32_t t,
                   (uint32_t)(seed >> 32));
 }
 
-// u = (top 23 bits + 1/2) * 2^-23, exact in fp32, in [2^-24, 1 - 2^-24].
+// u = (top 23 bits + 1/2) * 2^-23, exact in fp32, in [2^-24, 1 - 2^-24]: the float with
+// mantissa m = x >> 9 and exponent 0 is 1 + m 2^-23; subtracting 1 - 2^-24 (exact, the result
+// has at most 24 significant bits) leaves (m + 1/2) 2^-23.
 __device__ __forceinline__ float uniform01(uint32_t x) {
-  return ((float)(x >> 9) + 0.5f) * 0x1p-23f;
+  return __uint_as_float((x >> 9) | 0x3F800000u) - 0x1.fffffep-1f;
 }
 
 // Gumbel(0,1) sample -ln(-ln u): evaluated in fp64 and rounded once to fp32.

@@ -62,10 +62,10 @@ __device__ __forceinline__ void store_r4(void* R, int64_t idx, const float (&r)[
   }
 }
 
-template <typename T>
-__device__ __forceinline__ T exp_t(T x) {
-  if constexpr (std::is_same<T, double>::value) return exp(x); else return __expf(x);
-}
+// fp32 path: hardware exp2 / reciprocal / square root (about 1 ulp); fp64 path: libm.
+constexpr float kLog2e = 1.4426950408889634f;
+__device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+__device__ __forceinline__ float fast_sqrt(float x) { return __builtin_amdgcn_sqrtf(x); }
 
 // One coordinate's relaxed sample (Alg. 1): p = softmax((kappa l + g) / tau), with the
 // largest perturbed logit r subtracted first.  vp = sum_k p_k (c_k - c_r), so that the soft
@@ -94,9 +94,16 @@ __device__ __forceinline__ void soft_sample(const float (&l)[K], const float (&c
     if (b[k] > bmax) { bmax = b[k]; cr = (T)c[k]; }
   }
   T z = 0;
+  if constexpr (kF64) {
 #pragma unroll
-  for (int k = 0; k < K; ++k) { p[k] = exp_t<T>((b[k] - bmax) * inv_tau); z += p[k]; }
-  const T rz = T(1) / z;
+    for (int k = 0; k < K; ++k) { p[k] = exp((b[k] - bmax) * inv_tau); z += p[k]; }
+  } else {
+    const float s2 = inv_tau * kLog2e;   // exp(a) = exp2(a log2 e)
+#pragma unroll
+    for (int k = 0; k < K; ++k) { p[k] = __builtin_amdgcn_exp2f((b[k] - bmax) * s2); z += p[k]; }
+  }
+  T rz;
+  if constexpr (kF64) rz = T(1) / z; else rz = fast_rcp(z);
   vp = 0;
 #pragma unroll
   for (int k = 0; k < K; ++k) { p[k] *= rz; vp += p[k] * ((T)c[k] - cr); }
@@ -191,7 +198,9 @@ __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
         const T d = coef * p[k] * (((T)a.c[k] - cr) - vp);
         const T m1 = b1 * (T)f4get(mv[k], q) + omb1 * d;
         const T v1 = b2 * (T)f4get(vv[k], q) + omb2 * d * d;
-        const T l1 = (T)l[k] - step_l * m1 / (sqrt(v1) * rbc2 + eps);
+        T l1;
+        if constexpr (kF64) l1 = (T)l[k] - step_l * m1 / (sqrt(v1) * rbc2 + eps);
+        else l1 = (T)l[k] - step_l * m1 * fast_rcp(fast_sqrt(v1) * rbc2 + eps);
         f4set(mv[k], q, (float)m1);
         f4set(vv[k], q, (float)v1);
         f4set(lv[k], q, (float)l1);
@@ -218,7 +227,8 @@ __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
         const T step_s = kF64 ? (T)a.step_s_d : (T)a.step_s;
         const T m1 = b1 * (T)a.MS[sidx] + omb1 * ds_part;
         const T v1 = b2 * (T)a.VS[sidx] + omb2 * ds_part * ds_part;
-        s_new = (float)(s - step_s * m1 / (sqrt(v1) * rbc2 + eps));
+        if constexpr (kF64) s_new = (float)(s - step_s * m1 / (sqrt(v1) * rbc2 + eps));
+        else s_new = (float)(s - step_s * m1 * fast_rcp(fast_sqrt(v1) * rbc2 + eps));
         bad |= !(__builtin_isfinite(s_new) && __builtin_isfinite((float)v1));
         a.MS[sidx] = (float)m1;
         a.VS[sidx] = (float)v1;
