@@ -10,10 +10,13 @@ pure function of (seed, e, k, t) and both sides draw the same numbers.
 
 Counter layout (a reading of ours, stated once here):
     key     = (seed mod 2^32, seed >> 32)
-    counter = (e mod 2^32, e >> 32, t, stream * 256 + j)
     e       = global coordinate index ((b * O) + o) * I + i
-    j       = block of four levels: word r of block j feeds level k = 4 j + r
+    chunk   = the four coordinates e0 .. e0 + 3, e0 = e - e mod 4
     stream  = 0 for step noise, 1 for the initial logit noise of Eq. 4
+    The chunk's 4 K values (coordinate e0 + q, level k, at flat position f = q K + k) are
+    the words of K Philox calls: call j = f div 4 has counter
+    (e0 mod 2^32, e0 >> 32, t, stream * 256 + j), and position f takes its word f mod 4.
+    No word is drawn and left unused, whatever K is.
 
 Pinned by: rocRAND's host Philox4x32-10 (tests/test_oracle_rng.py), chi-square
 uniformity, Gumbel moments (mean = Euler-Mascheroni constant, variance pi^2/6),
@@ -59,17 +62,30 @@ def philox4x32_10(c0, c1, c2, c3, key):
 
 
 def raw_words(seed, e, t, stream, n_levels):
-    """uint32 words for coordinates ``e`` (int64 array), shape (len(e), n_levels)."""
-    e = np.asarray(e, dtype=np.uint64)
-    lo = (e & np.uint64(_MASK32)).astype(np.uint32)
-    hi = (e >> np.uint64(32)).astype(np.uint32)
-    out = np.empty((e.size, 4 * ((n_levels + 3) // 4)), dtype=np.uint32)
-    for j in range((n_levels + 3) // 4):
-        words = philox4x32_10(lo, hi, np.uint32(t & _MASK32),
-                              np.uint32(stream * 256 + j), seed)
-        for r in range(4):
-            out[:, 4 * j + r] = words[r]
-    return out[:, :n_levels]
+    """uint32 words for coordinates ``e`` (int64 array), shape (len(e), n_levels).
+
+    Follows the chunk layout above: coordinate e, level k sits at flat position
+    f = (e mod 4) K + k of its chunk's stream, i.e. word f mod 4 of call f div 4.
+    """
+    e = np.asarray(e, dtype=np.uint64).reshape(-1)
+    e0 = e - (e % np.uint64(4))
+    lo = (e0 & np.uint64(_MASK32)).astype(np.uint32)
+    hi = (e0 >> np.uint64(32)).astype(np.uint32)
+    q = (e % np.uint64(4)).astype(np.int64)
+    out = np.empty((e.size, n_levels), dtype=np.uint32)
+    calls = {}
+    for k in range(n_levels):
+        f = q * n_levels + k
+        j, w = f // 4, f % 4
+        for jj in np.unique(j):
+            if jj not in calls:
+                calls[jj] = philox4x32_10(lo, hi, np.uint32(t & _MASK32),
+                                          np.uint32(stream * 256 + int(jj)), seed)
+            sel = j == jj
+            for ww in range(4):
+                m = sel & (w == ww)
+                out[m, k] = calls[jj][ww][m]
+    return out
 
 
 def uniform(words):
@@ -94,15 +110,34 @@ def gumbel(seed, e, t, n_levels):
 def init_normals(seed, e, n_levels):
     """Standard normals for the initial logit noise of Eq. 4 (Box-Muller).
 
-    Words (x0, x1) of each Philox block give z = sqrt(-2 ln u0) cos(2 pi u1)
-    for level 4j and the matching sine for level 4j+1; words (x2, x3) give
-    levels 4j+2 and 4j+3.  Evaluated in float64, stored as float32.
+    In each chunk's word stream (stream 1, t = 0) the words at flat positions
+    (2m, 2m + 1) form one Box-Muller pair: position 2m takes
+    z = sqrt(-2 ln u_2m) cos(2 pi u_2m+1) and position 2m + 1 the matching sine.
+    A pair never straddles two Philox calls.  Evaluated in float64, stored as float32.
     """
-    u = uniform(raw_words(seed, e, 0, STREAM_INIT, 4 * ((n_levels + 3) // 4)))
-    z = np.empty_like(u)
-    for a in range(0, u.shape[1], 2):
-        rad = np.sqrt(-2.0 * np.log(u[:, a]))
-        ang = 2.0 * np.pi * u[:, a + 1]
-        z[:, a] = rad * np.cos(ang)
-        z[:, a + 1] = rad * np.sin(ang)
-    return np.float32(z[:, :n_levels]).astype(np.float64)
+    e = np.asarray(e, dtype=np.uint64).reshape(-1)
+    q = (e % np.uint64(4)).astype(np.int64)
+    e0 = e - (e % np.uint64(4))
+    z = np.empty((e.size, n_levels))
+    for k in range(n_levels):
+        f = q * n_levels + k
+        fk = [uniform(_word_at(seed, e0, STREAM_INIT, ff)) for ff in (f - (f & 1), f | 1)]
+        rad = np.sqrt(-2.0 * np.log(fk[0]))
+        ang = 2.0 * np.pi * fk[1]
+        z[:, k] = np.where(f & 1, rad * np.sin(ang), rad * np.cos(ang))
+    return np.float32(z).astype(np.float64)
+
+
+def _word_at(seed, e0, stream, f):
+    """Word at flat position ``f`` (array) of the stream of chunks starting at ``e0``."""
+    lo = (e0 & np.uint64(_MASK32)).astype(np.uint32)
+    hi = (e0 >> np.uint64(32)).astype(np.uint32)
+    out = np.empty(e0.size, dtype=np.uint32)
+    j, w = f // 4, f % 4
+    for jj in np.unique(j):
+        sel = j == jj
+        words = philox4x32_10(lo[sel], hi[sel], np.uint32(0), np.uint32(stream * 256 + int(jj)), seed)
+        for ww in range(4):
+            m = w[sel] == ww
+            out[np.flatnonzero(sel)[m]] = words[ww][m]
+    return out

@@ -23,12 +23,18 @@ __device__ __forceinline__ U4 philox10(U4 c, uint32_t k0, uint32_t k1) {
   return c;
 }
 
-// Counter of coordinate e, step t, stream (0 = step noise, 1 = initial logit noise), block j
-// of four levels: (e mod 2^32, e >> 32, t, stream*256 + j); key = seed.
-__device__ __forceinline__ U4 noise_words(uint64_t seed, uint64_t e, uint32_t t, uint32_t stream,
+// Noise layout: the four coordinates e0 .. e0+3 of an aligned chunk (e0 = e - e mod 4) read
+// their 4K values, coordinate e0+q / level k at flat position f = q K + k, from K Philox calls:
+// call j has counter (e0 mod 2^32, e0 >> 32, t, stream*256 + j) and position f takes word
+// f mod 4 of call f div 4.  stream 0 = step noise, 1 = initial logit noise; key = seed.
+__device__ __forceinline__ U4 noise_words(uint64_t seed, uint64_t e0, uint32_t t, uint32_t stream,
                                           uint32_t j) {
-  return philox10(U4{(uint32_t)e, (uint32_t)(e >> 32), t, stream * 256u + j}, (uint32_t)seed,
+  return philox10(U4{(uint32_t)e0, (uint32_t)(e0 >> 32), t, stream * 256u + j}, (uint32_t)seed,
                   (uint32_t)(seed >> 32));
+}
+
+__device__ __forceinline__ uint32_t word_of(const U4& w, int r) {
+  return r == 0 ? w.x : r == 1 ? w.y : r == 2 ? w.z : w.w;
 }
 
 // u = (top 23 bits + 1/2) * 2^-23, exact in fp32, in [2^-24, 1 - 2^-24]: the float with
@@ -58,16 +64,26 @@ __device__ __forceinline__ float gumbel(uint32_t x) {
   if constexpr (kExact) return gumbel_exact(x); else return gumbel_fast(x);
 }
 
-// The K Gumbel values of coordinate e at step t.
+// The 4 x K Gumbel values of the chunk starting at e0 (a multiple of 4) at step t.
 template <int K, bool kExact>
-__device__ __forceinline__ void draw_gumbel(float (&g)[K], uint64_t seed, uint64_t e, uint32_t t) {
+__device__ __forceinline__ void draw_chunk(float (&g)[4][K], uint64_t seed, uint64_t e0, uint32_t t) {
 #pragma unroll
-  for (int j = 0; j < (K + 3) / 4; ++j) {
-    const U4 w = noise_words(seed, e, t, 0u, (uint32_t)j);
-    const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+  for (int j = 0; j < K; ++j) {
+    const U4 w = noise_words(seed, e0, t, 0u, (uint32_t)j);
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
-      if (4 * j + r < K) g[4 * j + r] = gumbel<kExact>(ws[r]);
+    for (int r = 0; r < 4; ++r) g[(4 * j + r) / K][(4 * j + r) % K] = gumbel<kExact>(word_of(w, r));
+  }
+}
+
+// The K Gumbel values of one coordinate e at step t (any e; draws only the calls it needs).
+template <int K, bool kExact>
+__device__ __forceinline__ void draw_one(float (&g)[K], uint64_t seed, uint64_t e, uint32_t t) {
+  const uint64_t e0 = e & ~(uint64_t)3;
+  const int q = (int)(e & 3);
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const int f = q * K + k;
+    g[k] = gumbel<kExact>(word_of(noise_words(seed, e0, t, 0u, (uint32_t)(f >> 2)), f & 3));
   }
 }
 

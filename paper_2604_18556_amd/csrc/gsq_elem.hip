@@ -72,18 +72,10 @@ __device__ __forceinline__ float fast_sqrt(float x) { return __builtin_amdgcn_sq
 // level v = c_r + vp and c_k - v = (c_k - c_r) - vp keep full relative accuracy when one
 // level holds almost all the mass.
 template <int K, bool kF64>
-__device__ __forceinline__ void soft_sample(const float (&l)[K], const float (&c)[8], uint64_t seed,
-                                            uint64_t e, uint32_t t, bool noise, float kappa,
-                                            Real<kF64> inv_tau, Real<kF64> (&p)[K],
+__device__ __forceinline__ void soft_sample(const float (&l)[K], const float (&c)[8], const float (&g)[K],
+                                            float kappa, Real<kF64> inv_tau, Real<kF64> (&p)[K],
                                             Real<kF64>& vp, Real<kF64>& cr) {
   using T = Real<kF64>;
-  float g[K];
-  if (noise) {
-    draw_gumbel<K, kF64>(g, seed, e, t);
-  } else {
-#pragma unroll
-    for (int k = 0; k < K; ++k) g[k] = 0.f;
-  }
   T b[K];
 #pragma unroll
   for (int k = 0; k < K; ++k) b[k] = (T)kappa * (T)l[k] + (T)g[k];
@@ -109,6 +101,20 @@ __device__ __forceinline__ void soft_sample(const float (&l)[K], const float (&c
   for (int k = 0; k < K; ++k) { p[k] *= rz; vp += p[k] * ((T)c[k] - cr); }
 }
 
+// Noise of the thread's chunk of four coordinates (or zeros when sampling is off).
+template <int K, bool kF64>
+__device__ __forceinline__ void chunk_noise(float (&g)[4][K], const ElemArgs& a, uint64_t e0,
+                                            uint32_t t) {
+  if (a.noise) {
+    draw_chunk<K, kF64>(g, a.seed, e0, t);
+  } else {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int k = 0; k < K; ++k) g[q][k] = 0.f;
+  }
+}
+
 // ------------------------------------------------------------------ forward: R = W - s * v
 template <int K, bool kF64>
 __global__ __launch_bounds__(kBlock) void k_forward(ElemArgs a) {
@@ -127,6 +133,8 @@ __global__ __launch_bounds__(kBlock) void k_forward(ElemArgs a) {
     float4 lv[K];
 #pragma unroll
     for (int k = 0; k < K; ++k) lv[k] = *reinterpret_cast<const float4*>(a.L + k * a.N + e0);
+    float g[4][K];
+    chunk_noise<K, kF64>(g, a, (uint64_t)e0, a.t);
     float r[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -134,8 +142,7 @@ __global__ __launch_bounds__(kBlock) void k_forward(ElemArgs a) {
 #pragma unroll
       for (int k = 0; k < K; ++k) l[k] = f4get(lv[k], q);
       T p[K], vp, cr;
-      soft_sample<K, kF64>(l, a.c, a.seed, (uint64_t)(e0 + q), a.t, a.noise != 0, a.kappa, inv_tau,
-                           p, vp, cr);
+      soft_sample<K, kF64>(l, a.c, g[q], a.kappa, inv_tau, p, vp, cr);
       r[q] = (float)((T)w[q] - s * (cr + vp));
     }
     store_r4<kF64>(a.Rout, padded_index(a, row, col0), r);
@@ -182,14 +189,16 @@ __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
       for (int k = 0; k < K; ++k) lv[k] = mv[k] = vv[k] = make_float4(0.f, 0.f, 0.f, 0.f);
     }
     T ds_part = 0;
+    {
+    float g[4][K];
+    chunk_noise<K, kF64>(g, a, (uint64_t)e0, a.t);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       float l[K];
 #pragma unroll
       for (int k = 0; k < K; ++k) l[k] = f4get(lv[k], q);
       T p[K], vp, cr;
-      soft_sample<K, kF64>(l, a.c, a.seed, (uint64_t)(e0 + q), a.t, a.noise != 0, a.kappa, inv_tau,
-                           p, vp, cr);
+      soft_sample<K, kF64>(l, a.c, g[q], a.kappa, inv_tau, p, vp, cr);
       const T gq = (T)f4get(gv, q);
       ds_part += gq * (cr + vp);
       const T coef = kt * (gq * s);
@@ -205,6 +214,7 @@ __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
         f4set(vv[k], q, (float)v1);
         f4set(lv[k], q, (float)l1);
       }
+    }
     }
     if (active) {
 #pragma unroll
@@ -240,6 +250,8 @@ __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
       const T inv_tau_n = kF64 ? (T)a.inv_tau_n_d : (T)a.inv_tau_n;
       float w[4];
       load_w4(a.W, a.w_bf16, e0, w);
+      float g[4][K];
+      chunk_noise<K, kF64>(g, a, (uint64_t)e0, a.t_next);
       float r[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
@@ -247,8 +259,7 @@ __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
 #pragma unroll
         for (int k = 0; k < K; ++k) l[k] = f4get(lv[k], q);
         T p[K], vp, cr;
-        soft_sample<K, kF64>(l, a.c, a.seed, (uint64_t)(e0 + q), a.t_next, a.noise != 0, a.kappa_n,
-                             inv_tau_n, p, vp, cr);
+        soft_sample<K, kF64>(l, a.c, g[q], a.kappa_n, inv_tau_n, p, vp, cr);
         r[q] = (float)((T)w[q] - (T)s_new * (cr + vp));
       }
       store_r4<kF64>(a.Rout, padded_index(a, row, col0), r);
@@ -354,16 +365,16 @@ __global__ void k_init_logits(const void* W, int w_bf16, const float* S, float* 
     float eps[8];
     for (int k = 0; k < 8; ++k) eps[k] = 0.f;
     if (ic.noise) {
-      for (int j = 0; j < (ic.K + 3) / 4; ++j) {
-        const U4 x = noise_words(ic.seed, (uint64_t)e, 0u, 1u, (uint32_t)j);
-        const double u0 = uniform01(x.x), u1 = uniform01(x.y), u2 = uniform01(x.z),
-                     u3 = uniform01(x.w);
-        const double r0 = sqrt(-2.0 * log(u0)), a0 = 2.0 * M_PI * u1;
-        const double r1 = sqrt(-2.0 * log(u2)), a1 = 2.0 * M_PI * u3;
-        eps[(4 * j + 0) & 7] = (float)(r0 * cos(a0));
-        eps[(4 * j + 1) & 7] = (float)(r0 * sin(a0));
-        eps[(4 * j + 2) & 7] = (float)(r1 * cos(a1));
-        eps[(4 * j + 3) & 7] = (float)(r1 * sin(a1));
+      // flat positions (2m, 2m+1) of the chunk's stream form one Box-Muller pair (cos, sin)
+      const uint64_t e0 = (uint64_t)e & ~(uint64_t)3;
+      const int qq = (int)(e & 3);
+      for (int k = 0; k < ic.K; ++k) {
+        const int f = qq * ic.K + k;
+        const U4 x = noise_words(ic.seed, e0, 0u, 1u, (uint32_t)(f >> 2));
+        const int r0 = f & 2;   // the pair's first word within the call
+        const double u0 = uniform01(word_of(x, r0)), u1 = uniform01(word_of(x, r0 + 1));
+        const double rad = sqrt(-2.0 * log(u0)), ang = 2.0 * M_PI * u1;
+        eps[k] = (float)((f & 1) ? rad * sin(ang) : rad * cos(ang));
       }
     }
     for (int k = 0; k < ic.K; ++k)
@@ -492,7 +503,7 @@ __global__ void k_gumbel(uint64_t seed, int64_t e0, int64_t count, uint32_t t, f
   for (int64_t n = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; n < count;
        n += (int64_t)gridDim.x * blockDim.x) {
     float g[K];
-    draw_gumbel<K, kExact>(g, seed, (uint64_t)(e0 + n), t);
+    draw_one<K, kExact>(g, seed, (uint64_t)(e0 + n), t);
     for (int k = 0; k < K; ++k) out[n * K + k] = g[k];
   }
 }

@@ -37,8 +37,22 @@ def test_counter_layout_fields_all_reach_the_output():
                   philox.raw_words(8, np.array([5], np.int64), 3, 0, 8),
                   philox.raw_words(7 + 2**32, np.array([5], np.int64), 3, 0, 8)):
         assert np.all(other != base)
-    # levels 4..7 come from block j = 1, not from a shifted copy of block 0
+    # the levels of one coordinate come from different words, not from a shifted copy
     assert np.all(base[0, 4:] != base[0, :4])
+
+
+@pytest.mark.parametrize("K", [2, 3, 5, 8])
+def test_chunk_stream_layout(K):
+    """The 4 K values of an aligned chunk of four coordinates are the words of K calls, in
+    order: coordinate e0 + q, level k is word (qK + k) mod 4 of call (qK + k) div 4."""
+    seed, t, e0 = 99, 5, 4 * 1234567
+    got = philox.raw_words(seed, np.arange(e0, e0 + 4), t, 0, K).reshape(-1)
+    calls = [philox.philox4x32_10(e0, 0, t, j, seed) for j in range(K)]
+    want = np.array([int(c[r]) for c in calls for r in range(4)], dtype=np.uint32)
+    np.testing.assert_array_equal(got, want)
+    # every coordinate of the chunk agrees with a lookup of its own
+    for q in range(4):
+        np.testing.assert_array_equal(philox.raw_words(seed, [e0 + q], t, 0, K)[0], want[q * K:(q + 1) * K])
 
 
 def test_uniform_map_is_exact_and_uniform():
