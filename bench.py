@@ -33,12 +33,12 @@ PEAK_FP64_TFLOPS = 78.6        # fp64 vector (the FP32 precision accumulates in 
 DEFAULT_WORKLOAD = "attn-4096x4096-k3"
 
 
-def algorithmic_work(w, fused, want_loss, lr_scales):
+def algorithmic_work(w, fused, want_loss, lr_scales, lion=False):
     """Per-launch algorithmic bytes / flops of each step kernel (see the design notes).
 
     Per coordinate, bf16 W and R, fp32 logits / moments / gradient, K levels, groups of gs:
       forward   4K (logits) + 2 (W) + 2 (R)                      + 4/gs (scale)
-      backward  12K read + 12K write (logits, m, v) + 4 (G)      + scale state
+      backward  12K read + 12K write (logits, m, v; Lion: no v) + 4 (G) + scale state
                 + [fused] 2 (W) + 2 (next R)
       contract  2 O I^2 flops per layer
     """
@@ -47,9 +47,10 @@ def algorithmic_work(w, fused, want_loss, lr_scales):
         gs = 16
     n = B * O * I
     wb = 2 if w.precision == "bf16" else 4
-    scale_b = (24.0 if lr_scales > 0 else 4.0) / gs
+    state = 16 if lion else 24                  # bytes per level: logits, m (, v), read + write
+    scale_b = (state if lr_scales > 0 else 4.0) / gs
     fwd = n * (4 * K + 2 * wb + 4.0 / gs)
-    bwd = n * (24 * K + 4 + scale_b + (2 * wb if fused else 0))
+    bwd = n * (state * K + 4 + scale_b + (2 * wb if fused else 0))
     flops = 2.0 * B * O * I * I
     contract_bytes = n * (wb + 4 + (wb if want_loss else 0)) + B * I * I * wb
     return {"forward": ("hbm", fwd), "backward": ("hbm", bwd), "contract": ("flops", flops, contract_bytes)}
@@ -133,6 +134,8 @@ def main():
     ap.add_argument("--cpu-rows", type=int, default=512)
     ap.add_argument("--cpu-steps", type=int, default=3)
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--optimizer", choices=("adam", "lion"), default="adam",
+                    help="adam (default) or lion (the paper's optimiser; lr 1e-4, weight decay 1.0)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -167,6 +170,8 @@ def main():
 
     T = w.steps
     fused = not args.no_fuse
+    lion = args.optimizer == "lion"
+    opt_kw = dict(optimizer=B.OPT_LION, lr_logits=1e-4, weight_decay=1.0) if lion else {}
     loss = torch.zeros(w.batch, device=dev)
 
     def tau_at(t):
@@ -177,7 +182,7 @@ def main():
         for i in range(n):
             t = t0 + i
             p = B.StepParams(tau=tau_at(t), lr_scales=w.lr_scales,
-                             tau_next=tau_at(t + 1) if fused else 0.0)
+                             tau_next=tau_at(t + 1) if fused else 0.0, **opt_kw)
             layer.step(p, loss_out=loss if (t % args.loss_every == 0) else None)
 
     run(0, args.warmup)
@@ -206,7 +211,7 @@ def main():
     once = layer.timing_read(reset=True)
     layer.timing(False)
 
-    work = algorithmic_work(w, fused, args.loss_every == 1, w.lr_scales)
+    work = algorithmic_work(w, fused, args.loss_every == 1, w.lr_scales, lion)
     per_kernel = {}
     for name, (ms, cnt) in kern.items():
         if cnt == 0:
@@ -250,7 +255,7 @@ def main():
         "config": {"workload": w.name, "batch": w.batch, "out_features": w.out_features,
                    "in_features": w.in_features, "levels": len(w.levels), "group_size": w.group_size,
                    "layout": w.layout, "precision": w.precision, "calibration_tokens": w.tokens,
-                   "tau_schedule": f"linear 1.0 -> 0.05 over {T} steps", "optimizer": "adam",
+                   "tau_schedule": f"linear 1.0 -> 0.05 over {T} steps", "optimizer": args.optimizer,
                    "next_sample_fused": fused, "loss_every": args.loss_every, "parallelism": "none"},
         "roofline": roofline,
         "cpu_baseline": cpu,

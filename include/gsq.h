@@ -49,6 +49,7 @@ typedef enum {
 enum { GSQ_LAYOUT_GROUP = 0, GSQ_LAYOUT_SUPERBLOCK = 1 };
 enum { GSQ_PREC_FP32 = 0, GSQ_PREC_BF16 = 1 };
 enum { GSQ_DT_FP32 = 0, GSQ_DT_BF16 = 1 };
+enum { GSQ_OPT_ADAM = 0, GSQ_OPT_LION = 1 };
 #define GSQ_MAX_LEVELS 8
 
 /* Layer configuration (read at gsq_layer_init; copied). */
@@ -88,6 +89,12 @@ typedef struct {
                               of that step has already been drawn by this one, saving one
                               pass over the logits.  Results are identical either way.      */
   float   kappa_next;      /* logit scale of the next step (used when tau_next > 0)         */
+  int32_t optimizer;       /* GSQ_OPT_ADAM: Adam, bias-corrected (AdamW when weight_decay > 0,
+                              the paper's ablation, App. B); GSQ_OPT_LION: Lion, the paper's
+                              optimiser (§3.3): theta -= lr (sign(beta1 m + (1-beta1) g)
+                              + weight_decay theta), then m = beta2 m + (1-beta2) g; eps and
+                              the second moment are unused                                   */
+  float   weight_decay;    /* decoupled weight decay on logits and scales (>= 0)            */
 } gsq_step_params;
 
 /*

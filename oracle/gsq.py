@@ -99,13 +99,16 @@ class StepParams:
     beta2: float = 0.95
     eps: float = 1e-8
     gumbel_noise: bool = True
+    optimizer: str = "adam"            # "adam" (AdamW when weight_decay > 0) | "lion"
+    weight_decay: float = 0.0          # decoupled, on logits and scales
 
 
 def as_f32_params(prm):
     """The step's scalars as the float32 values the library receives."""
     f = lambda x: float(np.float32(x))
     return StepParams(f(prm.tau), f(prm.kappa), f(prm.lr_logits), f(prm.lr_scales),
-                      f(prm.beta1), f(prm.beta2), f(prm.eps), bool(prm.gumbel_noise))
+                      f(prm.beta1), f(prm.beta2), f(prm.eps), bool(prm.gumbel_noise),
+                      prm.optimizer, f(prm.weight_decay))
 
 
 @dataclass
@@ -318,10 +321,10 @@ def backward(cfg, G, s_coord, p, v, tau, kappa):
     return dlog, dscale
 
 
-def adam(theta, m, v, grad, lr, beta1, beta2, eps, n):
-    """Adam (Kingma & Ba, 2015), bias-corrected at step n >= 1, no weight decay.
+def adam(theta, m, v, grad, lr, beta1, beta2, eps, n, wd=0.0):
+    """Adam (Kingma & Ba, 2015), bias-corrected at step n >= 1; with wd > 0 the decoupled
+    weight decay of AdamW (Loshchilov & Hutter, 2019), the paper's ablation optimiser (App. B).
 
-    The paper's optimiser is Lion (§3.3); Adam is the variant this path builds.
     Arithmetic in float64 on the float32 state; results stored as float32.
     """
     th = np.asarray(theta, np.float64)
@@ -329,15 +332,36 @@ def adam(theta, m, v, grad, lr, beta1, beta2, eps, n):
     v1 = beta2 * np.asarray(v, np.float64) + (1.0 - beta2) * grad * grad
     mhat = m1 / (1.0 - beta1 ** n)
     vhat = v1 / (1.0 - beta2 ** n)
-    th1 = th - lr * mhat / (np.sqrt(vhat) + eps)
+    th1 = th - lr * (mhat / (np.sqrt(vhat) + eps) + wd * th)
     return th1.astype(np.float32), m1.astype(np.float32), v1.astype(np.float32)
+
+
+def lion(theta, m, grad, lr, beta1, beta2, wd=0.0):
+    """Lion (Chen et al., 2023), the paper's optimiser (§3.3, App. B): the step is the sign of
+    the interpolation beta1 m + (1 - beta1) g, plus decoupled weight decay; the single moment
+    then moves with beta2.  sign(0) = 0.  float64 arithmetic, float32 storage.
+    """
+    th = np.asarray(theta, np.float64)
+    m = np.asarray(m, np.float64)
+    c = beta1 * m + (1.0 - beta1) * grad
+    th1 = th - lr * (np.sign(c) + wd * th)
+    m1 = beta2 * m + (1.0 - beta2) * grad
+    return th1.astype(np.float32), m1.astype(np.float32)
+
+
+def update(prm, theta, m, v, grad, lr, n):
+    """The chosen optimiser's update of one parameter tensor: (theta, m, v) after the step."""
+    if prm.optimizer == "lion":
+        th1, m1 = lion(theta, m, grad, lr, prm.beta1, prm.beta2, prm.weight_decay)
+        return th1, m1, np.asarray(v, np.float32)
+    return adam(theta, m, v, grad, lr, prm.beta1, prm.beta2, prm.eps, n, prm.weight_decay)
 
 
 def step(cfg, W, Hs, st, prm, rows=None, want=False):
     """One GSQ optimisation step on state ``st`` (returns a new state, the loss).
 
     Order: noise -> soft sample -> residual -> contraction and loss -> gradient
-    -> Adam on logits and (if lr_scales > 0) scales; t -> t + 1.  The loss is
+    -> optimiser (Adam / AdamW / Lion) on logits and (if lr_scales > 0) scales; t -> t + 1.  The loss is
     the one of this step's sample, before the update.
 
     ``rows`` restricts the step to a subset of the rows of every layer (rows
@@ -369,12 +393,10 @@ def step(cfg, W, Hs, st, prm, rows=None, want=False):
         dlog, dsc = backward(cfg, G[None], s_coord[None], p[None], v[None], prm.tau, prm.kappa)
         dlog, dsc = dlog[0], dsc[0]
         losses[b] = L
-        th, m1, v1 = adam(lg, st.m[b], st.v[b], dlog, prm.lr_logits, prm.beta1, prm.beta2,
-                          prm.eps, n)
+        th, m1, v1 = update(prm, lg, st.m[b], st.v[b], dlog, prm.lr_logits, n)
         new.logits[b], new.m[b], new.v[b] = th, m1, v1
         if prm.lr_scales > 0:
-            ts, ms, vs = adam(sc, st.m_s[b], st.v_s[b], dsc, prm.lr_scales, prm.beta1, prm.beta2,
-                              prm.eps, n)
+            ts, ms, vs = update(prm, sc, st.m_s[b], st.v_s[b], dsc, prm.lr_scales, n)
             new.scales[b], new.m_s[b], new.v_s[b] = ts, ms, vs
         if want:
             for k, val in zip(inter, (g, p, v, R, G, dlog, dsc)):

@@ -247,6 +247,10 @@ static gsq_status validate_params(const gsq_layer* h, const gsq_step_params* p) 
   if (!(std::isfinite(p->eps) && p->eps > 0.f)) return fail(GSQ_EINVAL, "eps must be finite and > 0");
   if (!(std::isfinite(p->tau_next) && p->tau_next >= 0.f && std::isfinite(p->kappa_next)))
     return fail(GSQ_EINVAL, "tau_next must be finite and >= 0, kappa_next finite");
+  if (p->optimizer != GSQ_OPT_ADAM && p->optimizer != GSQ_OPT_LION)
+    return fail(GSQ_EINVAL, "unknown optimizer %d", p->optimizer);
+  if (!(std::isfinite(p->weight_decay) && p->weight_decay >= 0.f))
+    return fail(GSQ_EINVAL, "weight_decay must be finite and >= 0");
   if (h->cfg.layout == GSQ_LAYOUT_SUPERBLOCK && p->lr_scales != 0.f)
     return fail(GSQ_EUNSUPPORTED, "SUPERBLOCK scales stay on their 6-bit grid: lr_scales must be 0");
   return GSQ_OK;
@@ -279,6 +283,8 @@ gsq_status gsq_step(gsq_layer* h, const gsq_step_params* p, float* loss_out, hip
   const double n = (double)(L.t + 1);
   const double bc1 = 1.0 - std::pow((double)p->beta1, n);
   const double bc2 = 1.0 - std::pow((double)p->beta2, n);
+  a.lion = p->optimizer == GSQ_OPT_LION ? 1 : 0;
+  a.wd = p->weight_decay;
   a.lr = p->lr_logits;
   a.lr_s = p->lr_scales;
   a.b1 = p->beta1; a.b2 = p->beta2; a.eps = p->eps;

@@ -149,9 +149,32 @@ __global__ __launch_bounds__(kBlock) void k_forward(ElemArgs a) {
   }
 }
 
-// ------------------------------------------------------------------ gradient + Adam (+ next sample)
-// dL/dl_k = (kappa / tau) G s p_k (c_k - v); dL/ds = sum over the group of G v.  Adam with
-// bias correction at step n = t + 1.  With a.fuse, the sample of step t + 1 is drawn from
+// One parameter's optimiser update.  Adam: bias-corrected (step = lr / (1 - b1^n),
+// rbc2 = 1 / sqrt(1 - b2^n)), plus decoupled decay lr wd theta (AdamW).  Lion: the sign of
+// b1 m + (1 - b1) d, plus decoupled decay; the moment then moves with b2; v is untouched.
+template <bool kF64>
+__device__ __forceinline__ void opt_update(bool lion, Real<kF64> d, Real<kF64>& th, Real<kF64>& m,
+                                           Real<kF64>& v, Real<kF64> lr, Real<kF64> step,
+                                           Real<kF64> b1, Real<kF64> b2, Real<kF64> omb1,
+                                           Real<kF64> omb2, Real<kF64> rbc2, Real<kF64> eps,
+                                           Real<kF64> wd) {
+  using T = Real<kF64>;
+  if (lion) {
+    const T c = b1 * m + omb1 * d;
+    const T sg = (T)((c > T(0)) - (c < T(0)));
+    th = th - lr * (sg + wd * th);
+    m = b2 * m + omb2 * d;
+  } else {
+    m = b1 * m + omb1 * d;
+    v = b2 * v + omb2 * d * d;
+    if constexpr (kF64) th = th - (step * m / (sqrt(v) * rbc2 + eps) + lr * wd * th);
+    else th = th - (step * m * fast_rcp(fast_sqrt(v) * rbc2 + eps) + lr * wd * th);
+  }
+}
+
+// ------------------------------------------------------------------ gradient + update (+ next sample)
+// dL/dl_k = (kappa / tau) G s p_k (c_k - v); dL/ds = sum over the group of G v.  Adam (bias
+// correction at step n = t + 1) or Lion.  With a.fuse, the sample of step t + 1 is drawn from
 // the updated logits and scale and its residual written to a.Rout.
 template <int K, bool kF64, bool kScales>
 __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
@@ -165,6 +188,8 @@ __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
   const T eps = (T)a.eps;
   const T step_l = kF64 ? (T)a.step_l_d : (T)a.step_l;
   const T rbc2 = kF64 ? (T)a.rbc2_d : (T)a.rbc2;
+  const T lr = (T)a.lr, wd = (T)a.wd;
+  const bool lion = a.lion != 0;
   const int lpg = a.gs / 4;   // lanes per scale group
   const int64_t gpr = a.I / a.gs;
   bool bad = false;
@@ -182,7 +207,8 @@ __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
       for (int k = 0; k < K; ++k) {
         lv[k] = *reinterpret_cast<const float4*>(a.L + k * a.N + e0);
         mv[k] = *reinterpret_cast<const float4*>(a.M + k * a.N + e0);
-        vv[k] = *reinterpret_cast<const float4*>(a.V + k * a.N + e0);
+        vv[k] = lion ? make_float4(0.f, 0.f, 0.f, 0.f)
+                     : *reinterpret_cast<const float4*>(a.V + k * a.N + e0);
       }
     } else {
 #pragma unroll
@@ -205,14 +231,11 @@ __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
 #pragma unroll
       for (int k = 0; k < K; ++k) {
         const T d = coef * p[k] * (((T)a.c[k] - cr) - vp);
-        const T m1 = b1 * (T)f4get(mv[k], q) + omb1 * d;
-        const T v1 = b2 * (T)f4get(vv[k], q) + omb2 * d * d;
-        T l1;
-        if constexpr (kF64) l1 = (T)l[k] - step_l * m1 / (sqrt(v1) * rbc2 + eps);
-        else l1 = (T)l[k] - step_l * m1 * fast_rcp(fast_sqrt(v1) * rbc2 + eps);
+        T th = (T)l[k], m1 = (T)f4get(mv[k], q), v1 = (T)f4get(vv[k], q);
+        opt_update<kF64>(lion, d, th, m1, v1, lr, step_l, b1, b2, omb1, omb2, rbc2, eps, wd);
         f4set(mv[k], q, (float)m1);
         f4set(vv[k], q, (float)v1);
-        f4set(lv[k], q, (float)l1);
+        f4set(lv[k], q, (float)th);
       }
     }
     }
@@ -225,7 +248,7 @@ __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
                  __builtin_isfinite(vv[k].z) && __builtin_isfinite(vv[k].w));
         *reinterpret_cast<float4*>(a.L + k * a.N + e0) = lv[k];
         *reinterpret_cast<float4*>(a.M + k * a.N + e0) = mv[k];
-        *reinterpret_cast<float4*>(a.V + k * a.N + e0) = vv[k];
+        if (!lion) *reinterpret_cast<float4*>(a.V + k * a.N + e0) = vv[k];
       }
     }
     float s_new = s32;
@@ -235,10 +258,10 @@ __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
       const bool leader = active && (lane & (lpg - 1)) == 0;
       if (leader) {
         const T step_s = kF64 ? (T)a.step_s_d : (T)a.step_s;
-        const T m1 = b1 * (T)a.MS[sidx] + omb1 * ds_part;
-        const T v1 = b2 * (T)a.VS[sidx] + omb2 * ds_part * ds_part;
-        if constexpr (kF64) s_new = (float)(s - step_s * m1 / (sqrt(v1) * rbc2 + eps));
-        else s_new = (float)(s - step_s * m1 * fast_rcp(fast_sqrt(v1) * rbc2 + eps));
+        T th = s, m1 = (T)a.MS[sidx], v1 = (T)a.VS[sidx];
+        opt_update<kF64>(lion, ds_part, th, m1, v1, (T)a.lr_s, step_s, b1, b2, omb1, omb2, rbc2,
+                         eps, wd);
+        s_new = (float)th;
         bad |= !(__builtin_isfinite(s_new) && __builtin_isfinite((float)v1));
         a.MS[sidx] = (float)m1;
         a.VS[sidx] = (float)v1;

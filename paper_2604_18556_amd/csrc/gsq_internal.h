@@ -32,8 +32,9 @@ struct ElemArgs {
   int32_t noise;
   float kappa, inv_tau;       // fp32 path of the BF16 precision
   double inv_tau_d;           // fp64 path of the FP32 precision
-  // Adam
-  float lr, lr_s, b1, b2, eps, step_l, step_s, rbc2;  // step_* = lr / (1 - b1^n), rbc2 = 1/sqrt(1 - b2^n)
+  // optimiser: Adam (step_* = lr / (1 - b1^n), rbc2 = 1/sqrt(1 - b2^n)) or Lion; decoupled decay
+  int32_t lion;
+  float lr, lr_s, b1, b2, eps, step_l, step_s, rbc2, wd;
   double step_l_d, step_s_d, rbc2_d;
   // sample of the next step, drawn by the backward kernel when fuse != 0
   int32_t fuse;

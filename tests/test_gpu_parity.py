@@ -333,3 +333,54 @@ def test_full_size_attention_layer_on_sampled_rows(dev):
         assert_state_close(gst, st_new, inter["G"], 1e-3, t + 1, label=f"full-size step {t}")
         assert np.isfinite(loss.item()) and loss.item() > 0
         st = st_new
+
+
+# ------------------------------------------------------------------ Lion (§3.3) and AdamW (App. B)
+@pytest.mark.parametrize("opt", ["lion", "adamw"])
+@pytest.mark.parametrize("prec,O,I,K,gs,tau", [("fp32", 256, 256, 4, 128, 0.2),
+                                               ("bf16", 200, 384, 3, 128, 0.5),
+                                               ("bf16", 130, 512, 8, 64, 0.1)])
+def test_lion_and_adamw_single_step(dev, opt, prec, O, I, K, gs, tau):
+    levels = {3: L3, 4: L4, 8: L8}[K]
+    W, H = layer_inputs(O, I, bf16=prec == "bf16", seed=O + 3 * I)
+    rcfg = ref.Config(O, I, levels, gs, precision=prec, seed=6)
+    pair = Pair(rcfg, W, H, dev)
+    st = ref.init_layer(rcfg, W)
+    pair.put(st)
+    optimizer = B.OPT_LION if opt == "lion" else B.OPT_ADAM
+    prm = B.StepParams(tau=tau, lr_logits=1e-3 if opt == "lion" else 1e-2, lr_scales=5e-5,
+                       optimizer=optimizer, weight_decay=1.0 if opt == "lion" else 0.1)
+    loss = pair.step(prm)
+    _, G = pair.intermediates()
+    new, L, inter = ref.step(rcfg, W, pair.Hs, st, oracle_params(prm), want=True)
+    tol = TOL[prec]
+    assert np.all(np.abs(loss - L) <= tol * np.abs(L))
+    assert rel_err(G, inter["G"]) <= tol
+    got = pair.get()
+    # from zero moments both optimisers step along sign(G ...): the G = 0 exception applies
+    assert_state_close(got, new, inter["G"], tol, 1, label=f"{opt} {prec} K{K}")
+    beta = 0.95 if opt == "lion" else 0.9   # Lion's stored moment uses beta2
+    assert rel_err(got.m / (1 - np.float32(beta)), inter["dlogits"]) <= tol
+
+
+def test_lion_tiny_layer_trajectory(dev):
+    """40 Lion steps (lr 1e-3, weight decay 1.0 as in Tab. 7) on the fp32 tiny layer."""
+    w = inputs.WORKLOADS["tiny-256x256-k4"]
+    W, H = inputs.make_layer(w)
+    rcfg = ref.Config(256, 256, w.levels, 128, precision="fp32", seed=0)
+    pair = Pair(rcfg, W, H, dev)
+    st = ref.init_layer(rcfg, W)
+    T = 40
+    for t in range(T):
+        tau = ref.tau_schedule(t, T)
+        prm = B.StepParams(tau=tau, lr_logits=1e-3, lr_scales=5e-5, optimizer=B.OPT_LION,
+                           weight_decay=1.0, tau_next=ref.tau_schedule(t + 1, T) if t + 1 < T else 0.0)
+        lg = pair.step(prm)[0]
+        st, L = ref.step(rcfg, W, pair.Hs, st, oracle_params(prm))
+        assert abs(lg - L[0]) <= 1e-5 * abs(L[0]), (t, lg, L[0])
+    got = pair.get()
+    diff = np.argwhere(ref.harden(got.logits) != ref.harden(st.logits))
+    srt = np.sort(st.logits, -1)
+    for idx in diff:
+        assert (srt[..., -1] - srt[..., -2])[tuple(idx)] < 1e-4 * np.abs(st.logits).max(), idx
+    assert rel_err(got.logits, st.logits) <= 1e-5

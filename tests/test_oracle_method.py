@@ -241,6 +241,46 @@ def test_adam_matches_torch_optim_adam():
         np.testing.assert_allclose(cur, p.detach().numpy(), rtol=0, atol=2e-6)
 
 
+def test_adamw_matches_torch_optim_adamw():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(24)
+    th = rng.standard_normal(500).astype(np.float32)
+    m = np.zeros_like(th)
+    v = np.zeros_like(th)
+    p = torch.tensor(th.astype(np.float64), requires_grad=True)
+    opt = torch.optim.AdamW([p], lr=1e-2, betas=(0.9, 0.95), eps=1e-8, weight_decay=0.5)
+    cur = th
+    for n in range(1, 6):
+        gr = rng.standard_normal(500) * 10.0 ** rng.integers(-4, 1, 500)
+        cur, m, v = gsq.adam(cur, m, v, gr, 1e-2, 0.9, 0.95, 1e-8, n, wd=0.5)
+        p.grad = torch.tensor(gr)
+        opt.step()
+        np.testing.assert_allclose(cur, p.detach().numpy(), rtol=0, atol=2e-6)
+
+
+def test_lion_properties():
+    """Lion's defining properties (Chen et al., 2023): without momentum it is signSGD; every
+    step has size exactly lr; weight decay alone scales by (1 - lr wd); the sign follows the
+    beta1 interpolation, not the stored moment; the moment then moves with beta2."""
+    rng = np.random.default_rng(25)
+    th = rng.standard_normal(1000)
+    g = rng.standard_normal(1000)
+    t1, m1 = gsq.lion(th, np.zeros(1000), g, 0.01, 0.0, 0.0)
+    np.testing.assert_allclose(t1, th - 0.01 * np.sign(g), atol=1e-6)
+    np.testing.assert_allclose(m1, g, rtol=1e-6)
+    m = rng.standard_normal(1000)
+    t2, _ = gsq.lion(th, m, g, 0.01, 0.9, 0.99)
+    np.testing.assert_allclose(np.abs(t2 - th), 0.01, rtol=1e-4)
+    t3, _ = gsq.lion(th, np.zeros(1000), np.zeros(1000), 0.01, 0.9, 0.99, wd=2.0)
+    np.testing.assert_allclose(t3, th * (1 - 0.02), rtol=1e-6)
+    # moment and gradient of opposite signs: the step follows 0.9 m + 0.1 g
+    m4 = np.array([1.0, -1.0, 0.05, -0.05])
+    g4 = np.array([-5.0, 5.0, -5.0, 5.0])
+    t4, m4b = gsq.lion(np.zeros(4), m4, g4, 1.0, 0.9, 0.99)
+    np.testing.assert_array_equal(t4, -np.sign(0.9 * m4 + 0.1 * g4).astype(np.float32))
+    np.testing.assert_allclose(m4b, 0.99 * m4 + 0.01 * g4, rtol=1e-6)
+
+
 # ------------------------------------------------------------------ initialisation (Eq. 4, App. A)
 def test_init_logits_prior_and_noise():
     rng = np.random.default_rng(30)
