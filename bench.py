@@ -33,13 +33,13 @@ PEAK_FP64_TFLOPS = 78.6        # fp64 vector (the FP32 precision accumulates in 
 DEFAULT_WORKLOAD = "attn-4096x4096-k3"
 
 
-def algorithmic_work(w, fused, want_loss, lr_scales, lion=False):
+def algorithmic_work(w, fused, want_loss, lr_scales, lion=False, samples=1):
     """Per-launch algorithmic bytes / flops of each step kernel (see the design notes).
 
     Per coordinate, bf16 W and R, fp32 logits / moments / gradient, K levels, groups of gs:
       forward   4K (logits) + 2 (W) + 2 (R)                      + 4/gs (scale)
-      backward  12K read + 12K write (logits, m, v; Lion: no v) + 4 (G) + scale state
-                + [fused] 2 (W) + 2 (next R)
+      backward  12K read + 12K write (logits, m, v; Lion: no v) + 4 M (G of each of the
+                M samples) + scale state + [fused] 2 (W) + 2 (next R)
       contract  2 O I^2 flops per layer
     """
     B, O, I, K, gs = w.batch, w.out_features, w.in_features, len(w.levels), w.group_size
@@ -50,7 +50,7 @@ def algorithmic_work(w, fused, want_loss, lr_scales, lion=False):
     state = 16 if lion else 24                  # bytes per level: logits, m (, v), read + write
     scale_b = (state if lr_scales > 0 else 4.0) / gs
     fwd = n * (4 * K + 2 * wb + 4.0 / gs)
-    bwd = n * (state * K + 4 + scale_b + (2 * wb if fused else 0))
+    bwd = n * (state * K + 4 * samples + scale_b + (2 * wb if fused else 0))
     flops = 2.0 * B * O * I * I
     contract_bytes = n * (wb + 4 + (wb if want_loss else 0)) + B * I * I * wb
     return {"forward": ("hbm", fwd), "backward": ("hbm", bwd), "contract": ("flops", flops, contract_bytes)}
@@ -78,7 +78,7 @@ def measured_traffic(kernel, workload):
     return rec["bytes_per_launch"]
 
 
-def cpu_baseline(w, W, H, rows, steps, lr_scales):
+def cpu_baseline(w, W, H, rows, steps, lr_scales, opt_kw):
     """The oracle, untuned, on ``rows`` rows of the layer for ``steps`` steps (host cores)."""
     import numpy as np
     from oracle import gsq as ref
@@ -94,7 +94,7 @@ def cpu_baseline(w, W, H, rows, steps, lr_scales):
     st = ref.init_layer(rcfg, W, rows=sel)
     t0 = time.perf_counter()
     for t in range(steps):
-        prm = ref.StepParams(tau=ref.tau_schedule(t, w.steps), lr_scales=lr_scales)
+        prm = ref.StepParams(tau=ref.tau_schedule(t, w.steps), lr_scales=lr_scales, **opt_kw)
         st, _ = ref.step(rcfg, W, Hs, st, prm, rows=sel)
     sec = (time.perf_counter() - t0) / steps
     frac = len(sel) / w.out_features
@@ -136,6 +136,8 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--optimizer", choices=("adam", "lion"), default="adam",
                     help="adam (default) or lion (the paper's optimiser; lr 1e-4, weight decay 1.0)")
+    ap.add_argument("--samples", type=int, default=1,
+                    help="independent Gumbel draws averaged per step (gradient accumulation)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -182,7 +184,8 @@ def main():
         for i in range(n):
             t = t0 + i
             p = B.StepParams(tau=tau_at(t), lr_scales=w.lr_scales,
-                             tau_next=tau_at(t + 1) if fused else 0.0, **opt_kw)
+                             tau_next=tau_at(t + 1) if fused else 0.0, samples=args.samples,
+                             **opt_kw)
             layer.step(p, loss_out=loss if (t % args.loss_every == 0) else None)
 
     run(0, args.warmup)
@@ -211,7 +214,7 @@ def main():
     once = layer.timing_read(reset=True)
     layer.timing(False)
 
-    work = algorithmic_work(w, fused, args.loss_every == 1, w.lr_scales, lion)
+    work = algorithmic_work(w, fused, args.loss_every == 1, w.lr_scales, lion, args.samples)
     per_kernel = {}
     for name, (ms, cnt) in kern.items():
         if cnt == 0:
@@ -237,7 +240,10 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(w, W, Hd.cpu().numpy(), args.cpu_rows, args.cpu_steps, w.lr_scales)
+        ref_opt = dict(samples=args.samples)
+        if lion:
+            ref_opt.update(optimizer="lion", lr_logits=1e-4, weight_decay=1.0)
+        cpu = cpu_baseline(w, W, Hd.cpu().numpy(), args.cpu_rows, args.cpu_steps, w.lr_scales, ref_opt)
 
     out = {
         "metric": METRIC,
@@ -256,7 +262,8 @@ def main():
                    "in_features": w.in_features, "levels": len(w.levels), "group_size": w.group_size,
                    "layout": w.layout, "precision": w.precision, "calibration_tokens": w.tokens,
                    "tau_schedule": f"linear 1.0 -> 0.05 over {T} steps", "optimizer": args.optimizer,
-                   "next_sample_fused": fused, "loss_every": args.loss_every, "parallelism": "none"},
+                   "next_sample_fused": fused, "loss_every": args.loss_every,
+                   "samples_per_step": args.samples, "parallelism": "none"},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "kernels": per_kernel,

@@ -95,7 +95,15 @@ typedef struct {
                               + weight_decay theta), then m = beta2 m + (1-beta2) g; eps and
                               the second moment are unused                                   */
   float   weight_decay;    /* decoupled weight decay on logits and scales (>= 0)            */
+  int32_t samples;         /* M independent Gumbel draws this step, 0 or 1 = one draw, at most
+                              GSQ_MAX_SAMPLES: gradients and the reported loss are averaged
+                              over the M samples (§3.3, gradient accumulation with resampled
+                              noise).  Each extra sample costs one more forward pass and one
+                              more contraction; buffers for M samples are allocated on the
+                              first step that asks for them.                                  */
 } gsq_step_params;
+
+#define GSQ_MAX_SAMPLES 16
 
 /*
  * Create a layer.  W: device, batch x O x I row-major, fp32 or bf16 (w_dtype).
@@ -163,8 +171,8 @@ gsq_status gsq_set_state(gsq_layer* h, const float* logits, const float* m, cons
 
 /*
  * Intermediates of the most recent gsq_step (device pointers, either may be NULL):
- * residual R = W - W_hat of that step's sample, batch x O x I, in the precision's
- * type (fp32 or bf16); grad = dL/dW_hat = -2 R H, fp32 batch x O x I.
+ * residual R = W - W_hat of that step's (last) sample, batch x O x I, in the precision's
+ * type (fp32 or bf16); grad = dL/dW_hat = -2 R H of the same sample, fp32 batch x O x I.
  * GSQ_EINVAL if no step has run since init / set_state / harden.
  */
 gsq_status gsq_get_intermediates(gsq_layer* h, void* residual, float* grad, hipStream_t stream);

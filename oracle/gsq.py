@@ -101,6 +101,7 @@ class StepParams:
     gumbel_noise: bool = True
     optimizer: str = "adam"            # "adam" (AdamW when weight_decay > 0) | "lion"
     weight_decay: float = 0.0          # decoupled, on logits and scales
+    samples: int = 1                   # independent Gumbel draws averaged per step (§3.3)
 
 
 def as_f32_params(prm):
@@ -108,7 +109,7 @@ def as_f32_params(prm):
     f = lambda x: float(np.float32(x))
     return StepParams(f(prm.tau), f(prm.kappa), f(prm.lr_logits), f(prm.lr_scales),
                       f(prm.beta1), f(prm.beta2), f(prm.eps), bool(prm.gumbel_noise),
-                      prm.optimizer, f(prm.weight_decay))
+                      prm.optimizer, f(prm.weight_decay), max(1, int(prm.samples)))
 
 
 @dataclass
@@ -361,13 +362,17 @@ def step(cfg, W, Hs, st, prm, rows=None, want=False):
     """One GSQ optimisation step on state ``st`` (returns a new state, the loss).
 
     Order: noise -> soft sample -> residual -> contraction and loss -> gradient
-    -> optimiser (Adam / AdamW / Lion) on logits and (if lr_scales > 0) scales; t -> t + 1.  The loss is
-    the one of this step's sample, before the update.
+    -> optimiser (Adam / AdamW / Lion) on logits and (if lr_scales > 0) scales; t -> t + 1.
+    With prm.samples = M > 1 the noise is drawn M times independently and the gradients
+    (and the reported loss) are averaged over the M samples (§3.3, gradient accumulation
+    with resampled noise).  The loss is
+    taken before the update, averaged over the step's samples.
 
     ``rows`` restricts the step to a subset of the rows of every layer (rows
     are independent given H); ``st`` then holds just those rows and noise
     indices stay the global ones.
-    ``want`` returns the intermediates (g, p, v, R, G, dlogits, dscales).
+    ``want`` returns the intermediates (g, p, v, R, G of the last sample; the averaged
+    dlogits, dscales).
     """
     B, O, I, K = cfg.batch, cfg.out_features, cfg.in_features, cfg.K
     prm = as_f32_params(prm)
@@ -380,19 +385,25 @@ def step(cfg, W, Hs, st, prm, rows=None, want=False):
     inter = {k: [] for k in ("g", "p", "v", "R", "G", "dlogits", "dscales")}
     for b in range(B):
         e = coord_index(cfg, b, rows)
-        if prm.gumbel_noise:
-            g = philox.gumbel(cfg.seed, e, st.t, K).reshape(len(rows), I, K)
-        else:
-            g = np.zeros((len(rows), I, K))
         lg = st.logits[b]
         sc = st.scales[b]
         s_coord = expand_scales(sc, cfg.gs)
-        p, v, R = forward(cfg, W[b], lg, s_coord, g, prm.tau, prm.kappa)
-        P, L = contract(cfg, R, Hs[b])
-        G = -2.0 * P
-        dlog, dsc = backward(cfg, G[None], s_coord[None], p[None], v[None], prm.tau, prm.kappa)
-        dlog, dsc = dlog[0], dsc[0]
-        losses[b] = L
+        dlog = dsc = 0.0
+        for smp in range(prm.samples):
+            if prm.gumbel_noise:
+                g = philox.gumbel(cfg.seed, e, st.t, K, smp).reshape(len(rows), I, K)
+            else:
+                g = np.zeros((len(rows), I, K))
+            p, v, R = forward(cfg, W[b], lg, s_coord, g, prm.tau, prm.kappa)
+            P, L = contract(cfg, R, Hs[b])
+            G = -2.0 * P
+            dl1, ds1 = backward(cfg, G[None], s_coord[None], p[None], v[None], prm.tau, prm.kappa)
+            dlog = dlog + dl1[0]
+            dsc = dsc + ds1[0]
+            losses[b] += L
+        dlog = dlog / prm.samples
+        dsc = dsc / prm.samples
+        losses[b] /= prm.samples
         th, m1, v1 = update(prm, lg, st.m[b], st.v[b], dlog, prm.lr_logits, n)
         new.logits[b], new.m[b], new.v[b] = th, m1, v1
         if prm.lr_scales > 0:

@@ -13,10 +13,11 @@ Counter layout (a reading of ours, stated once here):
     e       = global coordinate index ((b * O) + o) * I + i
     chunk   = the four coordinates e0 .. e0 + 3, e0 = e - e mod 4
     stream  = 0 for step noise, 1 for the initial logit noise of Eq. 4
+    sample  = index m of an independent draw within one step (0 for a single draw)
     The chunk's 4 K values (coordinate e0 + q, level k, at flat position f = q K + k) are
     the words of K Philox calls: call j = f div 4 has counter
-    (e0 mod 2^32, e0 >> 32, t, stream * 256 + j), and position f takes its word f mod 4.
-    No word is drawn and left unused, whatever K is.
+    (e0 mod 2^32, e0 >> 32, t, (sample * 256 + stream) * 256 + j), and position f takes
+    its word f mod 4.  No word is drawn and left unused, whatever K is.
 
 Pinned by: rocRAND's host Philox4x32-10 (tests/test_oracle_rng.py), chi-square
 uniformity, Gumbel moments (mean = Euler-Mascheroni constant, variance pi^2/6),
@@ -61,7 +62,7 @@ def philox4x32_10(c0, c1, c2, c3, key):
     return c
 
 
-def raw_words(seed, e, t, stream, n_levels):
+def raw_words(seed, e, t, stream, n_levels, sample=0):
     """uint32 words for coordinates ``e`` (int64 array), shape (len(e), n_levels).
 
     Follows the chunk layout above: coordinate e, level k sits at flat position
@@ -80,7 +81,7 @@ def raw_words(seed, e, t, stream, n_levels):
         for jj in np.unique(j):
             if jj not in calls:
                 calls[jj] = philox4x32_10(lo, hi, np.uint32(t & _MASK32),
-                                          np.uint32(stream * 256 + int(jj)), seed)
+                                          np.uint32((sample * 256 + stream) * 256 + int(jj)), seed)
             sel = j == jj
             for ww in range(4):
                 m = sel & (w == ww)
@@ -97,13 +98,14 @@ def uniform(words):
     return ((np.asarray(words, dtype=np.uint32) >> np.uint32(9)).astype(np.float64) + 0.5) * 2.0 ** -23
 
 
-def gumbel(seed, e, t, n_levels):
+def gumbel(seed, e, t, n_levels, sample=0):
     """Gumbel(0,1) noise g = -ln(-ln u), evaluated in float64, stored as float32.
 
     Returns float64 values that are exactly float32-representable, shape
-    (len(e), n_levels).  Alg. 1 draws these once per logit per forward pass.
+    (len(e), n_levels).  Alg. 1 draws these once per logit per forward pass;
+    ``sample`` selects one of several independent draws of the same step.
     """
-    u = uniform(raw_words(seed, e, t, STREAM_STEP, n_levels))
+    u = uniform(raw_words(seed, e, t, STREAM_STEP, n_levels, sample))
     return np.float32(-np.log(-np.log(u))).astype(np.float64)
 
 

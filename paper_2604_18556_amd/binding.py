@@ -15,6 +15,7 @@ LAYOUT_GROUP, LAYOUT_SUPERBLOCK = 0, 1
 PREC_FP32, PREC_BF16 = 0, 1
 DT_FP32, DT_BF16 = 0, 1
 OPT_ADAM, OPT_LION = 0, 1
+MAX_SAMPLES = 16            # GSQ_MAX_SAMPLES
 STATUS_NAMES = {0: "GSQ_OK", -1: "GSQ_EINVAL", -2: "GSQ_ENOMEM", -3: "GSQ_EHIP",
                 -4: "GSQ_ENONFINITE", -5: "GSQ_EUNSUPPORTED"}
 
@@ -44,7 +45,8 @@ class CStepParams(ctypes.Structure):
                 ("lr_scales", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
                 ("eps", ctypes.c_float), ("gumbel_noise", ctypes.c_int32),
                 ("tau_next", ctypes.c_float), ("kappa_next", ctypes.c_float),
-                ("optimizer", ctypes.c_int32), ("weight_decay", ctypes.c_float)]
+                ("optimizer", ctypes.c_int32), ("weight_decay", ctypes.c_float),
+                ("samples", ctypes.c_int32)]
 
 
 @dataclass
@@ -91,11 +93,12 @@ class StepParams:
     kappa_next: float = 1.0
     optimizer: int = OPT_ADAM
     weight_decay: float = 0.0
+    samples: int = 1
 
     def to_c(self):
         return CStepParams(self.tau, self.kappa, self.lr_logits, self.lr_scales, self.beta1,
                            self.beta2, self.eps, 1 if self.gumbel_noise else 0, self.tau_next,
-                           self.kappa_next, self.optimizer, self.weight_decay)
+                           self.kappa_next, self.optimizer, self.weight_decay, self.samples)
 
 
 _lib = None

@@ -235,6 +235,27 @@ gsq_status gsq_layer_init(const gsq_config* cfg, const void* W, int32_t w_dtype,
   return GSQ_OK;
 }
 
+// Room for M per-sample gradients and loss partials (a step asking for more samples than
+// any before it); the old buffers are released after the device is idle.
+static gsq_status grow_sample_slots(gsq::Layer& L, int M) {
+  const size_t npad = (size_t)(L.B * L.Opad * L.Ipad);
+  float* G = nullptr;
+  double* part = nullptr;
+  if (!alloc(&G, (size_t)M * npad * 4) ||
+      !alloc(&part, (size_t)M * L.B * L.tiles_per_batch * 8)) {
+    if (G) (void)hipFree(G);
+    return fail(GSQ_ENOMEM, "no room for %d samples", M);
+  }
+  GSQ_HIP(hipDeviceSynchronize());   // no launch on any stream still reads the old buffers
+  (void)hipFree(L.G);
+  (void)hipFree(L.partials);
+  L.G = G;
+  L.partials = part;
+  L.sample_slots = M;
+  L.last = -1;
+  return GSQ_OK;
+}
+
 static gsq_status validate_params(const gsq_layer* h, const gsq_step_params* p) {
   if (!p) return fail(GSQ_EINVAL, "params is NULL");
   if (!(std::isfinite(p->tau) && p->tau > 0.f)) return fail(GSQ_EINVAL, "tau must be finite and > 0");
@@ -251,6 +272,8 @@ static gsq_status validate_params(const gsq_layer* h, const gsq_step_params* p) 
     return fail(GSQ_EINVAL, "unknown optimizer %d", p->optimizer);
   if (!(std::isfinite(p->weight_decay) && p->weight_decay >= 0.f))
     return fail(GSQ_EINVAL, "weight_decay must be finite and >= 0");
+  if (p->samples < 0 || p->samples > GSQ_MAX_SAMPLES)
+    return fail(GSQ_EINVAL, "samples must be in [0, %d]", GSQ_MAX_SAMPLES);
   if (h->cfg.layout == GSQ_LAYOUT_SUPERBLOCK && p->lr_scales != 0.f)
     return fail(GSQ_EUNSUPPORTED, "SUPERBLOCK scales stay on their 6-bit grid: lr_scales must be 0");
   return GSQ_OK;
@@ -263,6 +286,12 @@ gsq_status gsq_step(gsq_layer* h, const gsq_step_params* p, float* loss_out, hip
   if (st != GSQ_OK) return st;
   gsq::Layer& L = *h;
   if (L.t >= (int64_t)UINT32_MAX) return fail(GSQ_EINVAL, "step counter exhausted");
+  // grow the per-sample buffers before any launch argument captures their addresses
+  const int M = p->samples > 1 ? p->samples : 1;
+  if (M > L.sample_slots) {
+    gsq_status st2 = grow_sample_slots(L, M);
+    if (st2 != GSQ_OK) return st2;
+  }
   gsq::ElemArgs a = gsq::base_args(L);
   a.t = (uint32_t)L.t;
   a.noise = p->gumbel_noise ? 1 : 0;
@@ -272,13 +301,20 @@ gsq_status gsq_step(gsq_layer* h, const gsq_step_params* p, float* loss_out, hip
 
   const bool have = L.r_valid && L.r_t == L.t && L.r_tau == p->tau && L.r_kappa == p->kappa &&
                     L.r_noise == a.noise;
-  if (!have) {
-    a.Rout = L.R[L.cur];
-    GSQ_HIP(timed(L, GSQ_KERNEL_FORWARD, stream, [&] { return gsq::launch_forward(L, a, stream); }));
-  }
   const int use = L.cur;
-  GSQ_HIP(timed(L, GSQ_KERNEL_CONTRACT, stream, [&] { return gsq::launch_contract(L, L.R[use], loss_out != nullptr, stream); }));
-  if (loss_out) GSQ_HIP(timed(L, GSQ_KERNEL_REDUCE, stream, [&] { return gsq::launch_reduce_loss(L, loss_out, stream); }));
+  a.Rout = L.R[use];
+  for (int smp = 0; smp < M; ++smp) {
+    // sample 0 may have been drawn by the previous step; later samples reuse the buffer
+    if (smp > 0 || !have) {
+      a.sample = smp;
+      GSQ_HIP(timed(L, GSQ_KERNEL_FORWARD, stream, [&] { return gsq::launch_forward(L, a, stream); }));
+    }
+    GSQ_HIP(timed(L, GSQ_KERNEL_CONTRACT, stream, [&] { return gsq::launch_contract(L, L.R[use], loss_out != nullptr, smp, stream); }));
+  }
+  if (loss_out) GSQ_HIP(timed(L, GSQ_KERNEL_REDUCE, stream, [&] { return gsq::launch_reduce_loss(L, loss_out, M, stream); }));
+  a.sample = 0;
+  a.samples = M;
+  a.g_stride = L.B * L.Opad * L.Ipad;
 
   const double n = (double)(L.t + 1);
   const double bc1 = 1.0 - std::pow((double)p->beta1, n);
@@ -303,6 +339,7 @@ gsq_status gsq_step(gsq_layer* h, const gsq_step_params* p, float* loss_out, hip
   GSQ_HIP(timed(L, GSQ_KERNEL_BACKWARD, stream, [&] { return gsq::launch_backward(L, a, p->lr_scales > 0.f, stream); }));
 
   L.last = use;
+  L.last_sample = M - 1;
   L.t += 1;
   if (a.fuse) {
     L.cur = 1 - use;
@@ -333,9 +370,10 @@ gsq_status gsq_harden(gsq_layer* h, uint8_t* codes, float* scales, float* hard_l
   GSQ_HIP(timed(L, GSQ_KERNEL_HARDEN, stream, [&] { return gsq::launch_harden(L, codes ? codes : L.codes, Rh, stream); }));
   GSQ_HIP(timed(L, GSQ_KERNEL_HARDEN, stream, [&] { return gsq::launch_eff_scales(L, scales, stream); }));
   if (hard_loss_out) {
-    GSQ_HIP(timed(L, GSQ_KERNEL_CONTRACT, stream, [&] { return gsq::launch_contract(L, Rh, true, stream); }));
-    GSQ_HIP(timed(L, GSQ_KERNEL_REDUCE, stream, [&] { return gsq::launch_reduce_loss(L, hard_loss_out, stream); }));
+    GSQ_HIP(timed(L, GSQ_KERNEL_CONTRACT, stream, [&] { return gsq::launch_contract(L, Rh, true, 0, stream); }));
+    GSQ_HIP(timed(L, GSQ_KERNEL_REDUCE, stream, [&] { return gsq::launch_reduce_loss(L, hard_loss_out, 1, stream); }));
     L.last = -1;   // G now belongs to the hard residual
+    L.last_sample = 0;
   }
   return check_flag(h, stream);
 }
@@ -397,7 +435,8 @@ gsq_status gsq_get_intermediates(gsq_layer* h, void* residual, float* grad, hipS
   gsq::Layer& L = *h;
   if (L.last < 0) return fail(GSQ_EINVAL, "no step has run since init, set_state or harden");
   if (residual) GSQ_HIP(gsq::launch_copy_residual(L, L.R[L.last], residual, stream));
-  if (grad) GSQ_HIP(gsq::launch_copy_grad(L, L.G, grad, stream));
+  if (grad)
+    GSQ_HIP(gsq::launch_copy_grad(L, L.G + (int64_t)L.last_sample * L.B * L.Opad * L.Ipad, grad, stream));
   return GSQ_OK;
 }
 

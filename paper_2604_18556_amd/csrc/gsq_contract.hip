@@ -241,11 +241,14 @@ __global__ __launch_bounds__(256) void k_contract_f32(const float* __restrict__ 
     block_sum_to(lsum, partials + (b * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x);
 }
 
-// Loss of layer b = sum of its tile partials, in a fixed order.
-__global__ void k_reduce_loss(const double* partials, int64_t per_batch, float* loss_out, int* flag) {
+// Loss of layer b = mean over the samples of the sum of its tile partials, in a fixed order.
+// Partials of sample m, layer b start at (m * B + b) * per_batch.
+__global__ void k_reduce_loss(const double* partials, int64_t per_batch, int64_t B, int samples,
+                              float* loss_out, int* flag) {
   const int64_t b = blockIdx.x;
   double s = 0.0;
-  for (int64_t i = threadIdx.x; i < per_batch; i += 256) s += partials[b * per_batch + i];
+  for (int m = 0; m < samples; ++m)
+    for (int64_t i = threadIdx.x; i < per_batch; i += 256) s += partials[(m * B + b) * per_batch + i];
   __shared__ double red[256];
   red[threadIdx.x] = s;
   __syncthreads();
@@ -254,7 +257,7 @@ __global__ void k_reduce_loss(const double* partials, int64_t per_batch, float* 
     __syncthreads();
   }
   if (threadIdx.x == 0) {
-    const float L = (float)red[0];
+    const float L = (float)(red[0] / samples);
     loss_out[b] = L;
     if (!__builtin_isfinite(L)) *flag = 1;
   }
@@ -266,7 +269,9 @@ int64_t contract_tiles_per_batch(const Layer& L) {
   return L.bf16 ? (L.Opad / BM) * (L.Ipad / BN) : (L.Opad / TM) * (L.Ipad / TN);
 }
 
-hipError_t launch_contract(const Layer& L, const void* R, bool want_loss, hipStream_t s) {
+hipError_t launch_contract(const Layer& L, const void* R, bool want_loss, int slot, hipStream_t s) {
+  float* G = L.G + (int64_t)slot * L.B * L.Opad * L.Ipad;
+  double* partials = L.partials + (int64_t)slot * L.B * L.tiles_per_batch;
   if (L.bf16) {
     static bool attr_set = false;
     if (!attr_set) {
@@ -278,20 +283,20 @@ hipError_t launch_contract(const Layer& L, const void* R, bool want_loss, hipStr
     const int tiles_m = (int)(L.Opad / BM), tiles_n = (int)(L.Ipad / BN);
     dim3 grid((unsigned)(tiles_m * tiles_n), 1, (unsigned)L.B);
     hipLaunchKernelGGL(k_contract_bf16, grid, dim3(256), LDS_BYTES, s,
-                       static_cast<const uint16_t*>(R), static_cast<const uint16_t*>(L.H), L.G,
-                       L.partials, L.Opad, L.Ipad, tiles_m, tiles_n, want_loss ? 1 : 0);
+                       static_cast<const uint16_t*>(R), static_cast<const uint16_t*>(L.H), G,
+                       partials, L.Opad, L.Ipad, tiles_m, tiles_n, want_loss ? 1 : 0);
   } else {
     dim3 grid((unsigned)(L.Ipad / TN), (unsigned)(L.Opad / TM), (unsigned)L.B);
     hipLaunchKernelGGL(k_contract_f32, grid, dim3(256), 0, s, static_cast<const float*>(R),
-                       static_cast<const float*>(L.H), L.G, L.partials, L.Opad, L.Ipad,
+                       static_cast<const float*>(L.H), G, partials, L.Opad, L.Ipad,
                        want_loss ? 1 : 0);
   }
   return hipGetLastError();
 }
 
-hipError_t launch_reduce_loss(const Layer& L, float* loss_out, hipStream_t s) {
+hipError_t launch_reduce_loss(const Layer& L, float* loss_out, int samples, hipStream_t s) {
   hipLaunchKernelGGL(k_reduce_loss, dim3((unsigned)L.B), dim3(256), 0, s, L.partials,
-                     contract_tiles_per_batch(L), loss_out, L.flag);
+                     contract_tiles_per_batch(L), L.B, samples, loss_out, L.flag);
   return hipGetLastError();
 }
 

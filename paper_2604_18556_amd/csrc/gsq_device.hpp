@@ -25,11 +25,12 @@ __device__ __forceinline__ U4 philox10(U4 c, uint32_t k0, uint32_t k1) {
 
 // Noise layout: the four coordinates e0 .. e0+3 of an aligned chunk (e0 = e - e mod 4) read
 // their 4K values, coordinate e0+q / level k at flat position f = q K + k, from K Philox calls:
-// call j has counter (e0 mod 2^32, e0 >> 32, t, stream*256 + j) and position f takes word
-// f mod 4 of call f div 4.  stream 0 = step noise, 1 = initial logit noise; key = seed.
-__device__ __forceinline__ U4 noise_words(uint64_t seed, uint64_t e0, uint32_t t, uint32_t stream,
+// call j has counter (e0 mod 2^32, e0 >> 32, t, tag*256 + j) and position f takes word
+// f mod 4 of call f div 4.  tag = sample*256 + stream, stream 0 = step noise, 1 = initial logit
+// noise, sample = index of an independent draw within one step; key = seed.
+__device__ __forceinline__ U4 noise_words(uint64_t seed, uint64_t e0, uint32_t t, uint32_t tag,
                                           uint32_t j) {
-  return philox10(U4{(uint32_t)e0, (uint32_t)(e0 >> 32), t, stream * 256u + j}, (uint32_t)seed,
+  return philox10(U4{(uint32_t)e0, (uint32_t)(e0 >> 32), t, tag * 256u + j}, (uint32_t)seed,
                   (uint32_t)(seed >> 32));
 }
 
@@ -66,10 +67,11 @@ __device__ __forceinline__ float gumbel(uint32_t x) {
 
 // The 4 x K Gumbel values of the chunk starting at e0 (a multiple of 4) at step t.
 template <int K, bool kExact>
-__device__ __forceinline__ void draw_chunk(float (&g)[4][K], uint64_t seed, uint64_t e0, uint32_t t) {
+__device__ __forceinline__ void draw_chunk(float (&g)[4][K], uint64_t seed, uint64_t e0, uint32_t t,
+                                           uint32_t sample) {
 #pragma unroll
   for (int j = 0; j < K; ++j) {
-    const U4 w = noise_words(seed, e0, t, 0u, (uint32_t)j);
+    const U4 w = noise_words(seed, e0, t, sample * 256u, (uint32_t)j);
 #pragma unroll
     for (int r = 0; r < 4; ++r) g[(4 * j + r) / K][(4 * j + r) % K] = gumbel<kExact>(word_of(w, r));
   }

@@ -104,9 +104,9 @@ __device__ __forceinline__ void soft_sample(const float (&l)[K], const float (&c
 // Noise of the thread's chunk of four coordinates (or zeros when sampling is off).
 template <int K, bool kF64>
 __device__ __forceinline__ void chunk_noise(float (&g)[4][K], const ElemArgs& a, uint64_t e0,
-                                            uint32_t t) {
+                                            uint32_t t, uint32_t sample) {
   if (a.noise) {
-    draw_chunk<K, kF64>(g, a.seed, e0, t);
+    draw_chunk<K, kF64>(g, a.seed, e0, t, sample);
   } else {
 #pragma unroll
     for (int q = 0; q < 4; ++q)
@@ -134,7 +134,7 @@ __global__ __launch_bounds__(kBlock) void k_forward(ElemArgs a) {
 #pragma unroll
     for (int k = 0; k < K; ++k) lv[k] = *reinterpret_cast<const float4*>(a.L + k * a.N + e0);
     float g[4][K];
-    chunk_noise<K, kF64>(g, a, (uint64_t)e0, a.t);
+    chunk_noise<K, kF64>(g, a, (uint64_t)e0, a.t, (uint32_t)a.sample);
     float r[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -176,7 +176,7 @@ __device__ __forceinline__ void opt_update(bool lion, Real<kF64> d, Real<kF64>& 
 // dL/dl_k = (kappa / tau) G s p_k (c_k - v); dL/ds = sum over the group of G v.  Adam (bias
 // correction at step n = t + 1) or Lion.  With a.fuse, the sample of step t + 1 is drawn from
 // the updated logits and scale and its residual written to a.Rout.
-template <int K, bool kF64, bool kScales>
+template <int K, bool kF64, bool kScales, bool kMulti>
 __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
   using T = Real<kF64>;
   const int lane = threadIdx.x & 63;
@@ -199,10 +199,9 @@ __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
     const int64_t sidx = row * gpr + (active ? col0 / a.gs : 0);
     const float s32 = a.S[sidx];
     const T s = (T)s32;
-    float4 gv = make_float4(0.f, 0.f, 0.f, 0.f);
     float4 lv[K], mv[K], vv[K];
+    const int64_t gidx = active ? padded_index(a, row, col0) : 0;
     if (active) {
-      gv = *reinterpret_cast<const float4*>(a.G + padded_index(a, row, col0));
 #pragma unroll
       for (int k = 0; k < K; ++k) {
         lv[k] = *reinterpret_cast<const float4*>(a.L + k * a.N + e0);
@@ -214,31 +213,51 @@ __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
 #pragma unroll
       for (int k = 0; k < K; ++k) lv[k] = mv[k] = vv[k] = make_float4(0.f, 0.f, 0.f, 0.f);
     }
+    // gradient, averaged over the step's independent samples (one unless kMulti)
     T ds_part = 0;
-    {
-    float g[4][K];
-    chunk_noise<K, kF64>(g, a, (uint64_t)e0, a.t);
+    T dacc[4][K];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      float l[K];
+    for (int q = 0; q < 4; ++q)
 #pragma unroll
-      for (int k = 0; k < K; ++k) l[k] = f4get(lv[k], q);
-      T p[K], vp, cr;
-      soft_sample<K, kF64>(l, a.c, g[q], a.kappa, inv_tau, p, vp, cr);
-      const T gq = (T)f4get(gv, q);
-      ds_part += gq * (cr + vp);
-      const T coef = kt * (gq * s);
+      for (int k = 0; k < K; ++k) dacc[q][k] = 0;
+    const int M = kMulti ? a.samples : 1;
+    for (int smp = 0; smp < M; ++smp) {
+      const float4 gv = active ? *reinterpret_cast<const float4*>(a.G + smp * a.g_stride + gidx)
+                               : make_float4(0.f, 0.f, 0.f, 0.f);
+      float g[4][K];
+      chunk_noise<K, kF64>(g, a, (uint64_t)e0, a.t, (uint32_t)smp);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float l[K];
+#pragma unroll
+        for (int k = 0; k < K; ++k) l[k] = f4get(lv[k], q);
+        T p[K], vp, cr;
+        soft_sample<K, kF64>(l, a.c, g[q], a.kappa, inv_tau, p, vp, cr);
+        const T gq = (T)f4get(gv, q);
+        ds_part += gq * (cr + vp);
+        const T coef = kt * (gq * s);
+#pragma unroll
+        for (int k = 0; k < K; ++k) dacc[q][k] += coef * p[k] * (((T)a.c[k] - cr) - vp);
+      }
+    }
+    if constexpr (kMulti) {
+      const T inv_m = T(1) / (T)M;
+      ds_part *= inv_m;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int k = 0; k < K; ++k) dacc[q][k] *= inv_m;
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
 #pragma unroll
       for (int k = 0; k < K; ++k) {
-        const T d = coef * p[k] * (((T)a.c[k] - cr) - vp);
-        T th = (T)l[k], m1 = (T)f4get(mv[k], q), v1 = (T)f4get(vv[k], q);
-        opt_update<kF64>(lion, d, th, m1, v1, lr, step_l, b1, b2, omb1, omb2, rbc2, eps, wd);
+        T th = (T)f4get(lv[k], q), m1 = (T)f4get(mv[k], q), v1 = (T)f4get(vv[k], q);
+        opt_update<kF64>(lion, dacc[q][k], th, m1, v1, lr, step_l, b1, b2, omb1, omb2, rbc2, eps, wd);
         f4set(mv[k], q, (float)m1);
         f4set(vv[k], q, (float)v1);
         f4set(lv[k], q, (float)th);
       }
-    }
-    }
     if (active) {
 #pragma unroll
       for (int k = 0; k < K; ++k) {
@@ -274,7 +293,7 @@ __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
       float w[4];
       load_w4(a.W, a.w_bf16, e0, w);
       float g[4][K];
-      chunk_noise<K, kF64>(g, a, (uint64_t)e0, a.t_next);
+      chunk_noise<K, kF64>(g, a, (uint64_t)e0, a.t_next, 0u);
       float r[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
@@ -622,16 +641,22 @@ hipError_t launch_forward(const Layer& L, const ElemArgs& a, hipStream_t s) {
   }
 }
 
-template <int K>
-static hipError_t backward_k(const Layer& L, const ElemArgs& a, bool sc, hipStream_t s) {
+template <int K, bool kMulti>
+static void backward_km(const Layer& L, const ElemArgs& a, bool sc, hipStream_t s) {
   const dim3 g = row_grid(L), b(kBlock);
   if (L.bf16) {
-    if (sc) hipLaunchKernelGGL((k_backward<K, false, true>), g, b, 0, s, a);
-    else hipLaunchKernelGGL((k_backward<K, false, false>), g, b, 0, s, a);
+    if (sc) hipLaunchKernelGGL((k_backward<K, false, true, kMulti>), g, b, 0, s, a);
+    else hipLaunchKernelGGL((k_backward<K, false, false, kMulti>), g, b, 0, s, a);
   } else {
-    if (sc) hipLaunchKernelGGL((k_backward<K, true, true>), g, b, 0, s, a);
-    else hipLaunchKernelGGL((k_backward<K, true, false>), g, b, 0, s, a);
+    if (sc) hipLaunchKernelGGL((k_backward<K, true, true, kMulti>), g, b, 0, s, a);
+    else hipLaunchKernelGGL((k_backward<K, true, false, kMulti>), g, b, 0, s, a);
   }
+}
+
+template <int K>
+static hipError_t backward_k(const Layer& L, const ElemArgs& a, bool sc, hipStream_t s) {
+  if (a.samples > 1) backward_km<K, true>(L, a, sc, s);
+  else backward_km<K, false>(L, a, sc, s);
   return hipGetLastError();
 }
 

@@ -27,9 +27,12 @@ struct ElemArgs {
   int32_t O, I, Opad, Ipad, gs, w_bf16;
   uint64_t seed;
   float c[8];
-  // this step's sample
+  // this step's sample(s)
   uint32_t t;
   int32_t noise;
+  int32_t sample;             // forward: index of the independent draw
+  int32_t samples;            // backward: number of draws averaged (G of draw m at G + m * g_stride)
+  int64_t g_stride;
   float kappa, inv_tau;       // fp32 path of the BF16 precision
   double inv_tau_d;           // fp64 path of the FP32 precision
   // optimiser: Adam (step_* = lr / (1 - b1^n), rbc2 = 1/sqrt(1 - b2^n)) or Lion; decoupled decay
@@ -53,8 +56,10 @@ struct Layer {
   float *L = nullptr, *M = nullptr, *V = nullptr;
   float *S = nullptr, *MS = nullptr, *VS = nullptr;
   void* R[2] = {nullptr, nullptr};
-  float* G = nullptr;
-  double* partials = nullptr;
+  float* G = nullptr;          // one padded gradient per sample slot
+  double* partials = nullptr;  // loss partials, per sample slot
+  int sample_slots = 1;        // capacity of G and partials in samples
+  int last_sample = 0;         // slot holding the most recent step's last sample
   int64_t tiles_per_batch = 0;
   int* flag = nullptr;
   uint16_t* sb_d = nullptr;
@@ -94,7 +99,7 @@ ElemArgs base_args(const Layer& L);
 
 // ---- launchers (gsq_contract.hip)
 int64_t contract_tiles_per_batch(const Layer& L);
-hipError_t launch_contract(const Layer& L, const void* R, bool want_loss, hipStream_t s);
-hipError_t launch_reduce_loss(const Layer& L, float* loss_out, hipStream_t s);
+hipError_t launch_contract(const Layer& L, const void* R, bool want_loss, int slot, hipStream_t s);
+hipError_t launch_reduce_loss(const Layer& L, float* loss_out, int samples, hipStream_t s);
 
 }  // namespace gsq

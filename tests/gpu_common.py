@@ -83,7 +83,7 @@ class Pair:
 def oracle_params(p):
     return ref.StepParams(p.tau, p.kappa, p.lr_logits, p.lr_scales, p.beta1, p.beta2, p.eps,
                           p.gumbel_noise, "lion" if p.optimizer == B.OPT_LION else "adam",
-                          p.weight_decay)
+                          p.weight_decay, p.samples)
 
 
 def assert_state_close(gpu, orc, G_oracle, tol, n, label="", gate=None):

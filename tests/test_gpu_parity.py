@@ -384,3 +384,61 @@ def test_lion_tiny_layer_trajectory(dev):
     for idx in diff:
         assert (srt[..., -1] - srt[..., -2])[tuple(idx)] < 1e-4 * np.abs(st.logits).max(), idx
     assert rel_err(got.logits, st.logits) <= 1e-5
+
+
+@pytest.mark.parametrize("prec,O,I,K,gs,M", [
+    ("fp32", 256, 256, 4, 128, 2),
+    ("fp32", 70, 384, 3, 64, 3),
+    ("bf16", 200, 384, 3, 128, 4),
+    ("bf16", 130, 512, 8, 128, 2),
+])
+def test_multi_sample_step(dev, prec, O, I, K, gs, M):
+    """M independent Gumbel draws in one step, gradients and loss averaged (§3.3)."""
+    levels = {3: L3, 4: L4, 8: L8}[K]
+    W, H = layer_inputs(O, I, bf16=prec == "bf16", seed=O + 5 * I)
+    rcfg = ref.Config(O, I, levels, gs, precision=prec, seed=8)
+    pair = Pair(rcfg, W, H, dev)
+    st = _warm(ref.init_layer(rcfg, W), np.random.default_rng(I))
+    pair.put(st)
+    prm = B.StepParams(tau=0.3, lr_scales=5e-5, samples=M)
+    loss = pair.step(prm)
+    R, G = pair.intermediates()
+    new, L, inter = ref.step(rcfg, W, pair.Hs, st, oracle_params(prm), want=True)
+    tol = TOL[prec]
+    assert np.all(np.abs(loss - L) <= tol * np.abs(L)), (loss, L)
+    # the intermediates are those of the last sample
+    assert rel_err(G, inter["G"]) <= tol
+    assert rel_err(R, inter["R"]) <= (tol if prec == "fp32" else 2.0**-7)
+    # a single-sample oracle step differs: the averaging is really there
+    one, _ = ref.step(rcfg, W, pair.Hs, st, oracle_params(B.StepParams(tau=0.3, lr_scales=5e-5)))
+    assert rel_err(new.m, one.m) > 100 * tol
+    assert_state_close(pair.get(), new, inter["G"], tol, st.t + 1, label=f"M{M} {prec}")
+
+
+def test_multi_sample_count_changes_along_a_trajectory(dev):
+    """Steps with 2, 4, 1, 3 samples in turn (the per-sample buffers grow once, then are
+    reused) follow the oracle; the fused next-step draw is kept for sample 0."""
+    w = inputs.WORKLOADS["tiny-256x256-k4"]
+    W, H = inputs.make_layer(w)
+    rcfg = ref.Config(256, 256, w.levels, 128, precision="fp32", seed=2)
+    pair = Pair(rcfg, W, H, dev)
+    st = ref.init_layer(rcfg, W)
+    T = 8
+    for t, M in enumerate([2, 4, 1, 3, 1, 1, 4, 2]):
+        tau = ref.tau_schedule(t, T)
+        prm = B.StepParams(tau=tau, samples=M,
+                           tau_next=ref.tau_schedule(t + 1, T) if t + 1 < T else 0.0)
+        lg = pair.step(prm)[0]
+        st, L = ref.step(rcfg, W, pair.Hs, st, oracle_params(prm))
+        assert abs(lg - L[0]) <= 1e-5 * abs(L[0]), (t, M, lg, L[0])
+    got = pair.get()
+    assert rel_err(got.m, st.m) <= 1e-5 and rel_err(got.v, st.v) <= 1e-5
+
+
+def test_samples_out_of_range_rejected(dev):
+    w = inputs.WORKLOADS["tiny-256x256-k4"]
+    W, H = inputs.make_layer(w)
+    rcfg = ref.Config(256, 256, w.levels, 128, precision="fp32", seed=2)
+    pair = Pair(rcfg, W, H, dev)
+    with pytest.raises(RuntimeError, match="samples"):
+        pair.step(B.StepParams(tau=0.5, samples=B.MAX_SAMPLES + 1))

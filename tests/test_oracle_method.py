@@ -344,3 +344,51 @@ def test_a_planted_sign_error_in_the_backward_is_caught(monkeypatch):
     monkeypatch.setattr(gsq, "backward", wrong)
     with pytest.raises(AssertionError):
         test_backward_matches_central_finite_differences(1.0, 1.0)
+
+
+# ------------------------------------------------------------------ multi-sample averaging (§3.3)
+def _tiny_problem(seed=40):
+    rng = np.random.default_rng(seed)
+    O, I, K = 2, 16, 3
+    _, H = _spd(rng, I)
+    W = rng.normal(0, 0.02, (1, O, I))
+    cfg = gsq.Config(O, I, L3, 16, precision="fp64", seed=3)
+    st = _state(cfg, rng, spread=0.5)
+    return cfg, W, H, st
+
+
+def test_many_sample_gradient_matches_an_independent_monte_carlo_estimate():
+    """With M draws the averaged gradient estimates E_g[dL/dl]; numpy's own Gumbel generator
+    (an independent source) estimates the same expectation."""
+    cfg, W, H, st = _tiny_problem()
+    tau, M = 0.5, 3000
+    prm = gsq.StepParams(tau=tau, lr_scales=1e-5, samples=M)
+    _, _, inter = gsq.step(cfg, W, H, st, prm, want=True)
+    ours = inter["dlogits"][0]
+    rng = np.random.default_rng(77)
+    s_coord = gsq.expand_scales(st.scales[0], 16)
+    acc = []
+    for _ in range(M):
+        g = rng.gumbel(size=(2, 16, 3))
+        p, v, R = gsq.forward(cfg, W[0], st.logits[0], s_coord, g, tau, 1.0)
+        G = -2 * gsq.contract(cfg, R, H)[0]
+        acc.append(gsq.backward(cfg, G[None], s_coord[None], p[None], v[None], tau, 1.0)[0][0])
+    acc = np.stack(acc)
+    ref_mean, sem = acc.mean(0), acc.std(0) / np.sqrt(M)
+    # difference of two independent means: standard error sqrt(2) * sem
+    assert np.all(np.abs(ours - ref_mean) <= 6 * np.sqrt(2) * sem + 1e-12)
+
+
+def test_sample_averaging_divides_the_gradient_variance():
+    """Var of the M-sample gradient across steps (independent noise per step) ~ Var / M."""
+    cfg, W, H, st = _tiny_problem(41)
+    var = {}
+    for M in (1, 4):
+        grads = []
+        for t in range(150):
+            s = st.copy()
+            s.t = t
+            prm = gsq.StepParams(tau=0.5, samples=M)
+            grads.append(gsq.step(cfg, W, H, s, prm, want=True)[2]["dlogits"][0])
+        var[M] = np.stack(grads).var(0).sum()
+    assert 2.5 < var[1] / var[4] < 6.0, var[1] / var[4]
