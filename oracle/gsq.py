@@ -17,6 +17,14 @@ c_0 < ... < c_{K-1} (§3.2, Eq. 5); H = X^T X is the layer's calibration Gram
 matrix, so the reconstruction error of Eq. 1 for a linear layer is
 tr((W - W_hat) H (W - W_hat)^T).
 
+Three relaxations of a coordinate's choice (``Config.relaxation``):
+* "grid": one categorical over all K grid levels (§3.2, Eq. 5);
+* "shift": for wider grids, a categorical over the five index shifts
+  delta in {-2..2} around a fixed initial grid index j0, the level being
+  c[clip(j0 + delta)] (§3.2 "Higher bit-widths", Eq. 6);
+* "ternary": the mask x sign form of §3.1 (Eq. 2, Alg. 2), two binary
+  relaxations per coordinate with logits {-l, l} each.
+
 Readings where the paper is silent are listed in the design notes; each is
 repeated at the function that takes it.
 """
@@ -27,6 +35,10 @@ import numpy as np
 from . import philox
 
 F32 = np.float32
+
+RELAXATIONS = ("grid", "shift", "ternary")
+SHIFTS = np.array([-2, -1, 0, 1, 2])          # the local-shift window of §3.2 (Eq. 6)
+TERNARY_LEVELS = (-1.0, 0.0, 1.0)
 
 
 # ----------------------------------------------------------------------------- rounding helpers
@@ -67,19 +79,38 @@ class Config:
     """One layer (or a batch of independent layers, e.g. MoE experts)."""
     out_features: int
     in_features: int
-    levels: tuple                      # c_0 < ... < c_{K-1}
+    levels: tuple                      # the grid c_0 < ... < c_{n-1}
     group_size: int = 128              # gs, along the input dimension (§4.1)
     batch: int = 1
-    layout: str = "group"              # "group" | "superblock"
+    layout: str = "group"              # "group" | "superblock" | "base3" (3-level grids)
     precision: str = "fp32"            # "fp32" | "bf16" | "fp64": dtype of R and H in the contraction
     seed: int = 0
     alpha: float = 6.0                 # warm-start strength of Eq. 4 (Tab. 7: 6 for 2/3-bit)
     sigma_init: float = 1.0            # overall logit scale of Eq. 4
     init_noise: bool = True
+    relaxation: str = "grid"           # "grid" | "shift" | "ternary"
+
+    def __post_init__(self):
+        assert self.relaxation in RELAXATIONS, self.relaxation
+        if self.relaxation == "ternary":
+            assert tuple(float(c) for c in self.levels) == TERNARY_LEVELS
+        if self.layout == "base3":
+            assert len(self.levels) == 3
 
     @property
     def K(self):
+        """Logits per coordinate."""
+        return {"grid": len(self.levels), "shift": len(SHIFTS), "ternary": 2}[self.relaxation]
+
+    @property
+    def n_grid(self):
+        """Grid cardinality (the number of code values)."""
         return len(self.levels)
+
+    @property
+    def n_noise(self):
+        """Gumbel values per coordinate and draw: one per logit of each categorical."""
+        return 4 if self.relaxation == "ternary" else self.K
 
     @property
     def gs(self):
@@ -125,12 +156,14 @@ class State:
     sb_d: np.ndarray = None            # super-block fp16 d, (B, O, I // 256)
     sb_sc: np.ndarray = None           # super-block 6-bit sub-scales, (B, O, I // 16)
     extra: dict = field(default_factory=dict)
+    base: np.ndarray = None            # local shift: initial grid index j0, (B, O, I) uint8
 
     def copy(self):
         c = State(self.logits.copy(), self.m.copy(), self.v.copy(), self.scales.copy(),
                   self.m_s.copy(), self.v_s.copy(), self.t,
                   None if self.sb_d is None else self.sb_d.copy(),
-                  None if self.sb_sc is None else self.sb_sc.copy())
+                  None if self.sb_sc is None else self.sb_sc.copy(),
+                  base=None if self.base is None else self.base.copy())
         return c
 
 
@@ -210,17 +243,35 @@ def rtn_codes(W, s_coord, cfg):
 def prior_logits(q0, cfg):
     """Gaussian-prior warm-start logits (App. A), mean-subtracted per coordinate.
 
-    l_k = -(c_k - mu)^2 / 2 with mu = c_{q0}, then the mean over k is removed.
+    l_k = -(x_k - mu)^2 / 2 over the coordinate's candidates x_k, then the mean
+    over k is removed.  Full grid: x_k = c_k, mu = c_{q0}.  Local shift: the
+    candidates are the shifts themselves, x_k = delta_k, and mu = 0, since the
+    warm-start code is already the window's centre j0 (App. A).
     """
-    c = cfg.levels64()
-    mu = c[q0][..., None]
-    l = -0.5 * (c - mu) ** 2
+    if cfg.relaxation == "shift":
+        x = SHIFTS.astype(np.float64)
+        l = np.broadcast_to(-0.5 * x ** 2, np.shape(q0) + (len(x),))
+    else:
+        c = cfg.levels64()
+        mu = c[q0][..., None]
+        l = -0.5 * (c - mu) ** 2
     return l - l.mean(axis=-1, keepdims=True)
 
 
+def ternary_warm_logits(q0):
+    """Eq. 3: mask logit +1 where the warm-start code is non-zero, -1 where it is zero; sign
+    logit +1 / -1 for a +1 / -1 code and 0 for a zero code.  q0 indexes (-1, 0, 1).
+    Returns (..., 2) as (mask, sign)."""
+    val = np.asarray(q0).astype(np.int64) - 1
+    lm = np.where(val != 0, 1.0, -1.0)
+    lb = val.astype(np.float64)
+    return np.stack([lm, lb], axis=-1)
+
+
 def init_logits(q0, cfg, eps=None):
-    """Eq. 4: l = sigma_init * (eps + alpha * l_prior); eps ~ N(0, I) or zero."""
-    lp = prior_logits(q0, cfg)
+    """Eq. 4: l = sigma_init * (eps + alpha * l_warm); eps ~ N(0, I) or zero.  The warm
+    logits are App. A's prior (grid, shift) or Eq. 3's signs (ternary, not mean-subtracted)."""
+    lp = ternary_warm_logits(q0) if cfg.relaxation == "ternary" else prior_logits(q0, cfg)
     noise = 0.0 if eps is None else eps
     sigma, alpha = float(np.float32(cfg.sigma_init)), float(np.float32(cfg.alpha))
     return round_f32(sigma * (noise + alpha * lp)).astype(np.float32)
@@ -254,6 +305,8 @@ def init_layer(cfg, W, scales_init=None, rows=None):
     else:
         scales = group_absmax_scales(W, cfg)
     q0 = rtn_codes(W, expand_scales(scales, cfg.gs), cfg)
+    if cfg.n_grid > 255:
+        raise ValueError("grid too large")
     logits = np.empty((B, O, I, K), dtype=np.float32)
     for b in range(B):
         eps = None
@@ -265,6 +318,8 @@ def init_layer(cfg, W, scales_init=None, rows=None):
     zs = np.zeros_like(scales)
     st = State(logits, z, z.copy(), scales.astype(np.float32), zs, zs.copy(), 0, sb_d, sb_sc)
     st.extra["q0"] = q0
+    if cfg.relaxation == "shift":
+        st.base = q0.astype(np.uint8)
     return st
 
 
@@ -280,14 +335,32 @@ def soft_sample(logits, g, tau, kappa):
     return e / e.sum(axis=-1, keepdims=True)
 
 
-def forward(cfg, W, logits, s_coord, g, tau, kappa):
+def candidates(cfg, base=None):
+    """The values each logit stands for.
+
+    Full grid: the levels c_k (the same for every coordinate).  Local shift
+    (§3.2, Eq. 6): logit k of a coordinate with initial index j0 stands for the
+    grid level of index clip(j0 + delta_k, 0, n - 1) (the paper's 1-based
+    clip(j0 + delta, 1, 2^b)), so near the ends of the grid several shifts give
+    the same level.  Returns the levels (K,) or an array base.shape + (K,).
+    """
+    c = cfg.levels64()
+    if cfg.relaxation != "shift":
+        return c
+    j = np.clip(np.asarray(base, np.int64)[..., None] + SHIFTS, 0, cfg.n_grid - 1)
+    return c[j]
+
+
+def forward(cfg, W, logits, s_coord, g, tau, kappa, cand=None):
     """Soft weight and residual of one sample (Alg. 1 return value, scaled per §3.2).
 
     v = sum_k p_k c_k, W_hat = s * v, R = W - W_hat.  Returns (p, v, R) where R
-    is rounded to the contraction's input precision.
+    is rounded to the contraction's input precision.  ``cand`` holds the values
+    of the logits (``candidates``); default: the grid levels.
     """
     p = soft_sample(logits, g, tau, kappa)
-    v = (p * cfg.levels64()).sum(axis=-1)
+    c = cfg.levels64() if cand is None else cand
+    v = (p * c).sum(axis=-1)
     R = np.asarray(W, np.float64) - np.asarray(s_coord, np.float64) * v
     return p, v, to_contraction_precision(cfg, R)
 
@@ -303,7 +376,7 @@ def contract(cfg, R, Hs):
     return P, float((R * P).sum())
 
 
-def backward(cfg, G, s_coord, p, v, tau, kappa):
+def backward(cfg, G, s_coord, p, v, tau, kappa, cand=None):
     """Gradients of L with respect to the logits and the group scales.
 
     With W_hat = s v and G = dL/dW_hat:
@@ -313,13 +386,67 @@ def backward(cfg, G, s_coord, p, v, tau, kappa):
     one; the direct difference cancels to rounding noise once one level holds
     almost all the mass, which is the saturated regime App. B is about.
     """
-    c = cfg.levels64()
-    diff = (p[..., None, :] * (c[:, None] - c[None, :])).sum(axis=-1)    # [.., k] = sum_j p_j (c_k - c_j)
+    c = cfg.levels64() if cand is None else cand
+    c = np.broadcast_to(c, p.shape)
+    diff = (p[..., None, :] * (c[..., :, None] - c[..., None, :])).sum(axis=-1)   # [.., k] = sum_j p_j (c_k - c_j)
     dlog = (G * s_coord * (kappa / np.float64(tau)))[..., None] * p * diff
     gv = G * v
     B, O, I = gv.shape
     dscale = gv.reshape(B, O, I // cfg.gs, cfg.gs).sum(axis=-1)
     return dlog, dscale
+
+
+def binary_sample(logit, g2, tau, kappa):
+    """Alg. 1 on a two-element set with logits {-l, l} (§3): returns (p_first, p_second)."""
+    l = np.asarray(logit, np.float64)
+    p = soft_sample(np.stack([-l, l], axis=-1), g2, tau, kappa)
+    return p[..., 0], p[..., 1]
+
+
+def ternary_forward(cfg, W, logits, s_coord, g, tau, kappa):
+    """Ternary sample of Alg. 2: mask m~ = GS({0, 1}, {-l_m, l_m}), sign
+    b~ = GS({-1, 1}, {-l_b, l_b}), W_hat = s m~ b~ (Eq. 2).
+
+    ``logits`` (..., 2) holds (l_m, l_b); ``g`` (..., 4) the Gumbel noise of the mask's two
+    values then of the sign's two.  Returns (p, v, R): p (..., 2, 2) the two pairs of
+    probabilities, v = m~ b~ the soft level, R the residual in the contraction precision.
+    """
+    p0m, p1m = binary_sample(logits[..., 0], g[..., 0:2], tau, kappa)
+    p0b, p1b = binary_sample(logits[..., 1], g[..., 2:4], tau, kappa)
+    m = p1m                                  # 0 * p0 + 1 * p1
+    b = p1b - p0b                            # -1 * p0 + 1 * p1
+    v = m * b
+    R = np.asarray(W, np.float64) - np.asarray(s_coord, np.float64) * v
+    p = np.stack([np.stack([p0m, p1m], -1), np.stack([p0b, p1b], -1)], -2)
+    return p, v, to_contraction_precision(cfg, R)
+
+
+def ternary_backward(cfg, G, s_coord, p, tau, kappa):
+    """Gradients of the ternary sample.  With u = dL/dW_hat = G:
+      dL/dm~ = G s b~,  dL/db~ = G s m~;
+    each relaxed value y = sum_k p_k y_k of a pair with logits (-l, l) has
+      dy/dl = (kappa / tau) [p_1 (y_1 - y) - p_0 (y_0 - y)]        (softmax Jacobian);
+      dL/ds_g = sum_{i in g} G_i m~_i b~_i.
+    y_1 - y and y_0 - y are taken as p_0 (y_1 - y_0) and p_1 (y_0 - y_1) (the p's sum
+    to one), which keeps full relative accuracy when one value holds almost all the mass.
+    Returns dlogits (..., 2) = (d l_m, d l_b) and dscales.
+    """
+    kt = kappa / np.float64(tau)
+    p0m, p1m = p[..., 0, 0], p[..., 0, 1]
+    p0b, p1b = p[..., 1, 0], p[..., 1, 1]
+    m = p1m
+    b = p1b - p0b
+
+    def slope(p0, p1, y0, y1):
+        return kt * (p1 * (p0 * (y1 - y0)) - p0 * (p1 * (y0 - y1)))
+
+    dm_dl = slope(p0m, p1m, 0.0, 1.0)
+    db_dl = slope(p0b, p1b, -1.0, 1.0)
+    u = G * s_coord
+    dlog = np.stack([u * b * dm_dl, u * m * db_dl], axis=-1)
+    gv = G * m * b
+    B, O, I = gv.shape
+    return dlog, gv.reshape(B, O, I // cfg.gs, cfg.gs).sum(axis=-1)
 
 
 def adam(theta, m, v, grad, lr, beta1, beta2, eps, n, wd=0.0):
@@ -388,16 +515,25 @@ def step(cfg, W, Hs, st, prm, rows=None, want=False):
         lg = st.logits[b]
         sc = st.scales[b]
         s_coord = expand_scales(sc, cfg.gs)
+        cand = candidates(cfg, None if st.base is None else st.base[b])
+        nz = cfg.n_noise
         dlog = dsc = 0.0
         for smp in range(prm.samples):
             if prm.gumbel_noise:
-                g = philox.gumbel(cfg.seed, e, st.t, K, smp).reshape(len(rows), I, K)
+                g = philox.gumbel(cfg.seed, e, st.t, nz, smp).reshape(len(rows), I, nz)
             else:
-                g = np.zeros((len(rows), I, K))
-            p, v, R = forward(cfg, W[b], lg, s_coord, g, prm.tau, prm.kappa)
+                g = np.zeros((len(rows), I, nz))
+            if cfg.relaxation == "ternary":
+                p, v, R = ternary_forward(cfg, W[b], lg, s_coord, g, prm.tau, prm.kappa)
+            else:
+                p, v, R = forward(cfg, W[b], lg, s_coord, g, prm.tau, prm.kappa, cand)
             P, L = contract(cfg, R, Hs[b])
             G = -2.0 * P
-            dl1, ds1 = backward(cfg, G[None], s_coord[None], p[None], v[None], prm.tau, prm.kappa)
+            if cfg.relaxation == "ternary":
+                dl1, ds1 = ternary_backward(cfg, G[None], s_coord[None], p[None], prm.tau, prm.kappa)
+            else:
+                dl1, ds1 = backward(cfg, G[None], s_coord[None], p[None], v[None], prm.tau,
+                                    prm.kappa, None if cand.ndim == 1 else cand[None])
             dlog = dlog + dl1[0]
             dsc = dsc + ds1[0]
             losses[b] += L
@@ -422,6 +558,25 @@ def step(cfg, W, Hs, st, prm, rows=None, want=False):
 def harden(logits):
     """Hard codes q = argmax_k l_k, ties to the lowest k (the final step of Alg. 2, K-way)."""
     return np.argmax(np.asarray(logits), axis=-1).astype(np.uint8)
+
+
+def hard_codes(cfg, st):
+    """Grid codes of the hardened layer, per relaxation.
+
+    grid: argmax of the logits.  shift: clip(j0 + delta*) with delta* the
+    argmax shift.  ternary: the thresholds of Alg. 2, mask = [l_m >= 0] and
+    sign = +1 if l_b >= 0 else -1 (ties go to active and positive); the code
+    indexes (-1, 0, 1), i.e. 1 + mask * sign.
+    """
+    lg = np.asarray(st.logits)
+    if cfg.relaxation == "ternary":
+        mask = (lg[..., 0] >= 0).astype(np.int64)
+        sign = np.where(lg[..., 1] >= 0, 1, -1)
+        return (1 + mask * sign).astype(np.uint8)
+    k = harden(lg).astype(np.int64)
+    if cfg.relaxation == "shift":
+        return np.clip(st.base.astype(np.int64) + SHIFTS[k], 0, cfg.n_grid - 1).astype(np.uint8)
+    return k.astype(np.uint8)
 
 
 def scales_fp16(scales):
@@ -450,7 +605,7 @@ def hard_loss(cfg, W, Hs, codes, scales_eff):
 
 def harden_layer(cfg, W, Hs, st):
     """``gsq_harden``: codes, effective scales (fp16-rounded in the plain layout), hard loss."""
-    codes = harden(st.logits)
+    codes = hard_codes(cfg, st)
     if cfg.layout == "superblock":
         eff = st.scales.astype(np.float32)
     else:

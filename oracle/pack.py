@@ -19,8 +19,19 @@ the exact bytes are ours): every 256 consecutive weights of a row form one
     [codes: 256 x 3-bit, LSB-first, 96 bytes]
 records in row-major order.
 
+Base-3 layout (3-level grids, e.g. ternary, the 1.58-bit case of §3.1 and Tab. 1):
+    code section: the codes t in {0, 1, 2} of all coordinates in row-major order,
+        five per byte, byte n = sum_{j<5} t_{5n+j} 3^j (3^5 = 243 <= 256), the last
+        byte completed with zero codes: ceil(N / 5) bytes, 1.6 bits per weight;
+    scale section: as in the plain layout.
+Tab. 1 books ternary GSQ at 1.71 bits per parameter, which is the entropy
+log2(3) = 1.585 bits per code plus 16 bits per 128 weights; a byte-aligned base-3
+format cannot reach log2(3), and 5 codes per byte (1.6 + 0.125 = 1.725) is within
+1 % of it.
+
 Pinned by numpy.packbits(bitorder="little") on the expanded bit array, pack /
-unpack round trips, and the bits-per-parameter figures of Tab. 1.
+unpack round trips, Python integer arithmetic for the base-3 bytes, and the
+bits-per-parameter figures of Tab. 1.
 """
 import numpy as np
 
@@ -29,8 +40,11 @@ SUB = 16
 SB_BYTES = 2 + 12 + 96
 
 
+TRITS_PER_BYTE = 5
+
+
 def code_bits(K):
-    """ceil(log2 K) for 2 <= K <= 8."""
+    """ceil(log2 K) for 2 <= K <= 16."""
     return int(np.ceil(np.log2(K)))
 
 
@@ -109,3 +123,31 @@ def unpack_superblock(data, batch, O, I):
     sc = np.stack([_values_of(rec[r, 2:14], 6, 16) for r in range(n)]).astype(np.uint8)
     codes = np.stack([_values_of(rec[r, 14:110], 3, 256) for r in range(n)]).astype(np.uint8)
     return codes.reshape(batch, O, I), d, sc.reshape(batch, O, I // SUB)
+
+
+def packed_size_base3(batch, O, I, gs):
+    n = batch * O * I
+    return -(-n // TRITS_PER_BYTE) + 2 * batch * O * (I // gs)
+
+
+def pack_base3(codes, scales16):
+    """Base-3 layout: five codes per byte (see module doc), then float16 scales."""
+    codes = np.asarray(codes, dtype=np.uint8).reshape(-1)
+    assert int(codes.max(initial=0)) < 3
+    n = codes.size
+    padded = np.zeros(-(-n // TRITS_PER_BYTE) * TRITS_PER_BYTE, dtype=np.int64)
+    padded[:n] = codes
+    weights = 3 ** np.arange(TRITS_PER_BYTE, dtype=np.int64)
+    body = (padded.reshape(-1, TRITS_PER_BYTE) * weights).sum(axis=1).astype(np.uint8)
+    sc = np.asarray(scales16, dtype=np.float16).reshape(-1).astype("<f2").view(np.uint8)
+    return np.concatenate([body, sc])
+
+
+def unpack_base3(data, batch, O, I, gs):
+    n = batch * O * I
+    nb = -(-n // TRITS_PER_BYTE)
+    data = np.asarray(data, dtype=np.uint8)
+    body = data[:nb].astype(np.int64)
+    trits = np.stack([(body // 3 ** j) % 3 for j in range(TRITS_PER_BYTE)], axis=1).reshape(-1)[:n]
+    scales = data[nb:].copy().view("<f2").astype(np.float16).reshape(batch, O, I // gs)
+    return trits.astype(np.uint8).reshape(batch, O, I), scales
