@@ -40,17 +40,21 @@ def algorithmic_work(w, fused, want_loss, lr_scales, lion=False, samples=1):
       forward   4K (logits) + 2 (W) + 2 (R)                      + 4/gs (scale)
       backward  12K read + 12K write (logits, m, v; Lion: no v) + 4 M (G of each of the
                 M samples) + scale state + [fused] 2 (W) + 2 (next R)
+    K is the number of logits per coordinate (the grid size, 5 for the local shift, 2 for
+    the ternary mask and sign); the local shift also reads one byte of base index.
       contract  2 O I^2 flops per layer
     """
-    B, O, I, K, gs = w.batch, w.out_features, w.in_features, len(w.levels), w.group_size
+    B, O, I, gs = w.batch, w.out_features, w.in_features, w.group_size
+    K = {"shift": 5, "ternary": 2}.get(w.relaxation, len(w.levels))   # logits per coordinate
+    base = 1 if w.relaxation == "shift" else 0                        # u8 initial grid index
     if w.layout == "superblock":
         gs = 16
     n = B * O * I
     wb = 2 if w.precision == "bf16" else 4
-    state = 16 if lion else 24                  # bytes per level: logits, m (, v), read + write
+    state = 16 if lion else 24                  # bytes per logit: logits, m (, v), read + write
     scale_b = (state if lr_scales > 0 else 4.0) / gs
-    fwd = n * (4 * K + 2 * wb + 4.0 / gs)
-    bwd = n * (state * K + 4 * samples + scale_b + (2 * wb if fused else 0))
+    fwd = n * (4 * K + base + 2 * wb + 4.0 / gs)
+    bwd = n * (state * K + base + 4 * samples + scale_b + (2 * wb if fused else 0))
     flops = 2.0 * B * O * I * I
     contract_bytes = n * (wb + 4 + (wb if want_loss else 0)) + B * I * I * wb
     return {"forward": ("hbm", fwd), "backward": ("hbm", bwd), "contract": ("flops", flops, contract_bytes)}
@@ -88,7 +92,8 @@ def cpu_baseline(w, W, H, rows, steps, lr_scales, opt_kw):
     except Exception:
         threads = os.cpu_count()
     rcfg = ref.Config(w.out_features, w.in_features, w.levels, w.group_size, batch=w.batch,
-                      layout=w.layout, precision=w.precision, seed=0)
+                      layout=w.layout, precision=w.precision, seed=0, relaxation=w.relaxation,
+                      alpha=3.0 if w.relaxation == "ternary" else 6.0)
     sel = np.arange(min(rows, w.out_features))
     Hs = ref.symmetrize(H)
     st = ref.init_layer(rcfg, W, rows=sel)
@@ -162,8 +167,11 @@ def main():
     if w.precision == "bf16":
         Wd = Wd.to(torch.bfloat16)
     cfg = B.LayerConfig(w.out_features, w.in_features, w.levels, w.group_size, w.batch,
-                        B.LAYOUT_SUPERBLOCK if w.layout == "superblock" else B.LAYOUT_GROUP,
-                        B.PREC_BF16 if w.precision == "bf16" else B.PREC_FP32, seed=0)
+                        {"superblock": B.LAYOUT_SUPERBLOCK, "base3": B.LAYOUT_BASE3}.get(w.layout, B.LAYOUT_GROUP),
+                        B.PREC_BF16 if w.precision == "bf16" else B.PREC_FP32, seed=0,
+                        alpha=3.0 if w.relaxation == "ternary" else 6.0,
+                        relaxation={"shift": B.RELAX_SHIFT, "ternary": B.RELAX_TERNARY}.get(
+                            w.relaxation, B.RELAX_GRID))
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     layer = B.Layer(cfg, Wd, Hd)
@@ -260,7 +268,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "batch": w.batch, "out_features": w.out_features,
                    "in_features": w.in_features, "levels": len(w.levels), "group_size": w.group_size,
-                   "layout": w.layout, "precision": w.precision, "calibration_tokens": w.tokens,
+                   "layout": w.layout, "precision": w.precision, "relaxation": w.relaxation,
+                   "calibration_tokens": w.tokens,
                    "tau_schedule": f"linear 1.0 -> 0.05 over {T} steps", "optimizer": args.optimizer,
                    "next_sample_fused": fused, "loss_every": args.loss_every,
                    "samples_per_step": args.samples, "parallelism": "none"},

@@ -46,24 +46,40 @@ typedef enum {
   GSQ_EUNSUPPORTED = -5   /* valid request the library does not implement              */
 } gsq_status;
 
-enum { GSQ_LAYOUT_GROUP = 0, GSQ_LAYOUT_SUPERBLOCK = 1 };
+enum { GSQ_LAYOUT_GROUP = 0, GSQ_LAYOUT_SUPERBLOCK = 1, GSQ_LAYOUT_BASE3 = 2 };
 enum { GSQ_PREC_FP32 = 0, GSQ_PREC_BF16 = 1 };
 enum { GSQ_DT_FP32 = 0, GSQ_DT_BF16 = 1 };
 enum { GSQ_OPT_ADAM = 0, GSQ_OPT_LION = 1 };
-#define GSQ_MAX_LEVELS 8
+
+/* How a coordinate's choice of grid level is relaxed.
+ * GRID:    one categorical over all n_levels levels (Alg. 1 over the grid of Eq. 5, §3.2);
+ *          n_levels logits per coordinate, 2 <= n_levels <= 8.
+ * SHIFT:   the local-shift relaxation of §3.2 (Eq. 6) for wider grids: 5 logits per
+ *          coordinate over the index shifts delta = -2..2 around a fixed initial index j0
+ *          (the round-to-nearest code); logit k stands for the level
+ *          c[clip(j0 + delta_k, 0, n_levels - 1)].  2 <= n_levels <= 16.
+ * TERNARY: the mask x sign form of §3.1 (Eq. 2, Alg. 2): two logits per coordinate, l_m and
+ *          l_b, each relaxed as a two-value Gumbel-Softmax with logits {-l, l}; the soft
+ *          weight is s m~ b~ with m~ over {0, 1} and b~ over {-1, 1}.  Levels must be exactly
+ *          {-1, 0, 1}; codes index them. */
+enum { GSQ_RELAX_GRID = 0, GSQ_RELAX_SHIFT = 1, GSQ_RELAX_TERNARY = 2 };
+#define GSQ_MAX_LEVELS 16
+#define GSQ_SHIFT_WINDOW 5
 
 /* Layer configuration (read at gsq_layer_init; copied). */
 typedef struct {
   int32_t  batch;          /* independent layers sharing the configuration (>= 1)           */
   int32_t  out_features;   /* O (>= 1)                                                      */
   int32_t  in_features;    /* I; multiple of group_size (GROUP) or of 256 (SUPERBLOCK)      */
-  int32_t  n_levels;       /* K, 2..8: grid cardinality |G_b| of Eq. 5                      */
-  float    levels[GSQ_MAX_LEVELS]; /* c_0 < ... < c_{K-1}, finite, not all zero              */
-  int32_t  group_size;     /* GROUP: 16, 32, 64, 128 or 256 consecutive inputs per scale;
-                              SUPERBLOCK: ignored (16-weight sub-blocks)                    */
-  int32_t  layout;         /* GSQ_LAYOUT_*: GROUP = one fp16 scale per group (Tab. 1 format);
-                              SUPERBLOCK = 256-weight records of 16 sub-blocks, each with a
-                              6-bit scale times one fp16 scale per record (K-quant style, §4.4) */
+  int32_t  n_levels;       /* n: grid cardinality |G_b| of Eq. 5 (limits per relaxation)    */
+  float    levels[GSQ_MAX_LEVELS]; /* c_0 < ... < c_{n-1}, finite, not all zero              */
+  int32_t  group_size;     /* GROUP, BASE3: 16, 32, 64, 128 or 256 consecutive inputs per
+                              scale; SUPERBLOCK: ignored (16-weight sub-blocks)             */
+  int32_t  layout;         /* GSQ_LAYOUT_*: GROUP = b-bit codes and one fp16 scale per group
+                              (Tab. 1 format); SUPERBLOCK = 256-weight records of 16
+                              sub-blocks, each with a 6-bit scale times one fp16 scale per
+                              record (K-quant style, §4.4; n_levels <= 8); BASE3 = as GROUP
+                              but five 3-level codes per byte (n_levels == 3, 1.6 bits)     */
   int32_t  precision;      /* GSQ_PREC_*: type of the residual R and of H in the contraction.
                               BF16: bf16 operands, fp32 accumulation on the matrix cores,
                               fp32 elementwise arithmetic with hardware log/exp.
@@ -72,6 +88,12 @@ typedef struct {
   float    alpha;          /* warm-start strength of Eq. 4 (the paper uses 6 for 2/3-bit)   */
   float    sigma_init;     /* overall logit scale of Eq. 4                                  */
   int32_t  init_noise;     /* 1: add N(0,1) noise to the initial logits (Eq. 4); 0: none    */
+  int32_t  relaxation;     /* GSQ_RELAX_*; the initial logits follow the warm start of each:
+                              GRID: App. A's Gaussian prior -(c_k - c_q0)^2/2 around the
+                              round-to-nearest code q0; SHIFT: the prior -delta^2/2 centred at
+                              delta = 0 (App. A, b > 2), j0 = q0; TERNARY: Eq. 3's +-1 / 0
+                              mask and sign logits of q0.  Then l = sigma_init (eps + alpha
+                              prior) (Eq. 4; GRID and SHIFT priors are mean-subtracted).    */
 } gsq_config;
 
 /* Scalars of one optimisation step (host values; the schedule lives with the caller). */
@@ -120,19 +142,21 @@ gsq_status gsq_layer_init(const gsq_config* cfg, const void* W, int32_t w_dtype,
                           const float* scales_init, hipStream_t stream, gsq_layer** out);
 
 /*
- * One optimisation step (Alg. 1 sample, Eq. 1 loss, gradient, Adam; the paper's
- * Alg. 2 loop body generalised to K levels by §3.2): draws g for step t, forms
- * the soft weight s * sum_k p_k c_k, the residual R, P = R H, the loss
- * tr(R H R^T), the gradients of the logits and scales, applies Adam (bias
- * correction at step t+1) and advances t.  loss_out: device fp32[batch]
- * receiving the loss of this step's sample before the update, or NULL to skip
- * computing it.
+ * One optimisation step (Alg. 1 sample, Eq. 1 loss, gradient, optimiser; the loop body of
+ * Alg. 2, generalised to n levels by §3.2): draws g for step t, forms the soft weight
+ * (GRID, SHIFT: s * sum_k p_k c_k over the coordinate's candidate levels; TERNARY:
+ * s m~ b~), the residual R, P = R H, the loss tr(R H R^T), the gradients of the logits
+ * and scales, applies the optimiser (bias correction at step t+1) and advances t.
+ * loss_out: device fp32[batch] receiving the loss of this step's sample(s) before the
+ * update, or NULL to skip computing it.
  */
 gsq_status gsq_step(gsq_layer* h, const gsq_step_params* p, float* loss_out, hipStream_t stream);
 
 /*
- * Harden (the final argmax of Alg. 2, K-way): codes q = argmax_k logits (ties to the
- * lowest k) into `codes` (device u8, batch x O x I, or NULL); effective scales
+ * Harden (the final step of Alg. 2): codes into `codes` (device u8, batch x O x I, or NULL),
+ * code = grid level index.  GRID: argmax_k logits (ties to the lowest k); SHIFT:
+ * clip(j0 + delta*) with delta* the argmax shift (ties to the lowest); TERNARY: mask
+ * l_m >= 0 and sign + if l_b >= 0 else -, code 1 + mask * sign.  Effective scales
  * into `scales` (device fp32, batch x O x (I/group_size) -- GROUP: the fp16-rounded
  * scales, SUPERBLOCK: d * sc per 16-weight sub-block; or NULL); the hard loss
  * tr(R H R^T) with R = W - s c[q] into hard_loss_out (device fp32[batch], or NULL).
@@ -143,14 +167,17 @@ gsq_status gsq_harden(gsq_layer* h, uint8_t* codes, float* scales, float* hard_l
                       hipStream_t stream);
 
 /* Bytes gsq_pack writes for this configuration (0 if the configuration is invalid).
- * GROUP: batch*O*I*b/8 code bytes (b = ceil(log2 K)) + 2*batch*O*(I/group_size) scale bytes;
- * SUPERBLOCK: 110 bytes per 256 weights. */
+ * GROUP: batch*O*I*b/8 code bytes (b = ceil(log2 n_levels)) + 2*batch*O*(I/group_size) scale
+ * bytes; BASE3: ceil(batch*O*I/5) code bytes + the same scale bytes; SUPERBLOCK: 110 bytes per
+ * 256 weights. */
 size_t gsq_packed_size(const gsq_config* cfg);
 
 /*
  * Pack the hardened layer into `packed` (device, >= gsq_packed_size bytes).
  * GROUP: one little-endian bitstream of b-bit codes (code = level index) over all
- * coordinates in row-major order, then the fp16 scales row-major.  SUPERBLOCK: per
+ * coordinates in row-major order, then the fp16 scales row-major.  BASE3: the codes
+ * t in {0, 1, 2} in row-major order, five per byte, byte n = sum_j t_{5n+j} 3^j (the last
+ * byte padded with zero codes), then the fp16 scales row-major.  SUPERBLOCK: per
  * 256 consecutive weights of a row, [fp16 d][16 x 6-bit sc, LSB first][256 x 3-bit
  * codes, LSB first] = 110 bytes, records row-major.  Synchronises the stream.
  */
@@ -158,16 +185,19 @@ gsq_status gsq_pack(gsq_layer* h, void* packed, size_t packed_bytes, hipStream_t
 
 /*
  * Copy the optimiser state out (device pointers, any may be NULL):
- * logits, m, v: fp32 batch x O x I x K; scales, m_s, v_s: fp32 batch x O x (I/gs)
- * (gs = 16 for SUPERBLOCK); t: host int64.  Synchronises the stream.
+ * logits, m, v: fp32 batch x O x I x K with K the logits per coordinate (GRID: n_levels,
+ * SHIFT: 5, TERNARY: 2 as (l_m, l_b)); scales, m_s, v_s: fp32 batch x O x (I/gs)
+ * (gs = 16 for SUPERBLOCK); base: SHIFT only, u8 batch x O x I, the initial grid index j0
+ * of every coordinate (must be NULL otherwise); t: host int64.  Synchronises the stream.
  */
 gsq_status gsq_get_state(gsq_layer* h, float* logits, float* m, float* v, float* scales,
-                         float* m_s, float* v_s, int64_t* t, hipStream_t stream);
+                         float* m_s, float* v_s, uint8_t* base, int64_t* t, hipStream_t stream);
 
-/* Overwrite the state (same layouts; NULL leaves that part unchanged; t >= 0). */
+/* Overwrite the state (same layouts; NULL leaves that part unchanged; t >= 0; every base
+ * index must be < n_levels, which the kernels do not check). */
 gsq_status gsq_set_state(gsq_layer* h, const float* logits, const float* m, const float* v,
-                         const float* scales, const float* m_s, const float* v_s, int64_t t,
-                         hipStream_t stream);
+                         const float* scales, const float* m_s, const float* v_s,
+                         const uint8_t* base, int64_t t, hipStream_t stream);
 
 /*
  * Intermediates of the most recent gsq_step (device pointers, either may be NULL):
@@ -179,8 +209,9 @@ gsq_status gsq_get_intermediates(gsq_layer* h, void* residual, float* grad, hipS
 
 /*
  * The Gumbel noise the step kernels draw (Alg. 1): g for the `count` coordinates
- * starting at global index e0 (e = ((b*O)+o)*I + i) at step t, K values each,
- * into g_out (device fp32, count x K).  Uses cfg's seed, n_levels and precision
+ * starting at global index e0 (e = ((b*O)+o)*I + i) at step t, Z values each, into g_out
+ * (device fp32, count x Z), Z = the logits per coordinate (GRID: n_levels, SHIFT: 5) or 4
+ * for TERNARY (the mask's two values, then the sign's two).  Uses cfg's seed and precision
  * (FP32: -ln(-ln u) evaluated in fp64 and rounded; BF16: hardware log2).
  */
 gsq_status gsq_gumbel(const gsq_config* cfg, int64_t e0, int64_t count, int64_t t, float* g_out,

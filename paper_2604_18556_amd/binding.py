@@ -11,7 +11,10 @@ from dataclasses import dataclass, field
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libgsq.so")
 
 GSQ_OK, GSQ_EINVAL, GSQ_ENOMEM, GSQ_EHIP, GSQ_ENONFINITE, GSQ_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
-LAYOUT_GROUP, LAYOUT_SUPERBLOCK = 0, 1
+LAYOUT_GROUP, LAYOUT_SUPERBLOCK, LAYOUT_BASE3 = 0, 1, 2
+RELAX_GRID, RELAX_SHIFT, RELAX_TERNARY = 0, 1, 2
+MAX_LEVELS = 16             # GSQ_MAX_LEVELS
+SHIFT_WINDOW = 5            # GSQ_SHIFT_WINDOW
 PREC_FP32, PREC_BF16 = 0, 1
 DT_FP32, DT_BF16 = 0, 1
 OPT_ADAM, OPT_LION = 0, 1
@@ -34,10 +37,10 @@ class GsqError(RuntimeError):
 class CConfig(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("out_features", ctypes.c_int32),
                 ("in_features", ctypes.c_int32), ("n_levels", ctypes.c_int32),
-                ("levels", ctypes.c_float * 8), ("group_size", ctypes.c_int32),
+                ("levels", ctypes.c_float * MAX_LEVELS), ("group_size", ctypes.c_int32),
                 ("layout", ctypes.c_int32), ("precision", ctypes.c_int32),
                 ("seed", ctypes.c_uint64), ("alpha", ctypes.c_float), ("sigma_init", ctypes.c_float),
-                ("init_noise", ctypes.c_int32)]
+                ("init_noise", ctypes.c_int32), ("relaxation", ctypes.c_int32)]
 
 
 class CStepParams(ctypes.Structure):
@@ -62,6 +65,7 @@ class LayerConfig:
     alpha: float = 6.0
     sigma_init: float = 1.0
     init_noise: bool = True
+    relaxation: int = RELAX_GRID
 
     def to_c(self):
         c = CConfig()
@@ -72,11 +76,17 @@ class LayerConfig:
         c.group_size, c.layout, c.precision = self.group_size, self.layout, self.precision
         c.seed, c.alpha, c.sigma_init = self.seed, self.alpha, self.sigma_init
         c.init_noise = 1 if self.init_noise else 0
+        c.relaxation = self.relaxation
         return c
 
     @property
     def gs(self):
         return 16 if self.layout == LAYOUT_SUPERBLOCK else self.group_size
+
+    @property
+    def K(self):
+        """Logits per coordinate."""
+        return {RELAX_SHIFT: SHIFT_WINDOW, RELAX_TERNARY: 2}.get(self.relaxation, len(self.levels))
 
 
 @dataclass
@@ -121,8 +131,8 @@ def load(path=None):
     lib.gsq_packed_size.argtypes = [ctypes.POINTER(CConfig)]
     lib.gsq_packed_size.restype = sz
     lib.gsq_pack.argtypes = [vp, vp, sz, vp]
-    lib.gsq_get_state.argtypes = [vp, vp, vp, vp, vp, vp, vp, ctypes.POINTER(i64), vp]
-    lib.gsq_set_state.argtypes = [vp, vp, vp, vp, vp, vp, vp, i64, vp]
+    lib.gsq_get_state.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, ctypes.POINTER(i64), vp]
+    lib.gsq_set_state.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i64, vp]
     lib.gsq_get_intermediates.argtypes = [vp, vp, vp, vp]
     lib.gsq_gumbel.argtypes = [ctypes.POINTER(CConfig), i64, i64, i64, vp, vp]
     lib.gsq_check.argtypes = [vp, vp]
@@ -204,15 +214,18 @@ class Layer:
         _check(load().gsq_pack(self.handle, _ptr(out), out.numel() * out.element_size(),
                                _stream(stream)))
 
-    def get_state(self, logits=None, m=None, v=None, scales=None, m_s=None, v_s=None, stream=None):
+    def get_state(self, logits=None, m=None, v=None, scales=None, m_s=None, v_s=None, base=None,
+                  stream=None):
         t = ctypes.c_int64()
         _check(load().gsq_get_state(self.handle, _ptr(logits), _ptr(m), _ptr(v), _ptr(scales),
-                                    _ptr(m_s), _ptr(v_s), ctypes.byref(t), _stream(stream)))
+                                    _ptr(m_s), _ptr(v_s), _ptr(base), ctypes.byref(t),
+                                    _stream(stream)))
         return t.value
 
-    def set_state(self, t, logits=None, m=None, v=None, scales=None, m_s=None, v_s=None, stream=None):
+    def set_state(self, t, logits=None, m=None, v=None, scales=None, m_s=None, v_s=None, base=None,
+                  stream=None):
         _check(load().gsq_set_state(self.handle, _ptr(logits), _ptr(m), _ptr(v), _ptr(scales),
-                                    _ptr(m_s), _ptr(v_s), int(t), _stream(stream)))
+                                    _ptr(m_s), _ptr(v_s), _ptr(base), int(t), _stream(stream)))
 
     def intermediates(self, residual=None, grad=None, stream=None):
         _check(load().gsq_get_intermediates(self.handle, _ptr(residual), _ptr(grad), _stream(stream)))

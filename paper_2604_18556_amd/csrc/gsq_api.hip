@@ -36,14 +36,27 @@ gsq_status hip_fail(hipError_t e, const char* what) {
 
 int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
-int code_bits(int K) { return K <= 2 ? 1 : K <= 4 ? 2 : 3; }
+int code_bits(int n) { return n <= 2 ? 1 : n <= 4 ? 2 : n <= 8 ? 3 : 4; }
+
+int logits_per_coord(const gsq_config& c) {
+  return c.relaxation == GSQ_RELAX_SHIFT ? GSQ_SHIFT_WINDOW
+         : c.relaxation == GSQ_RELAX_TERNARY ? 2 : c.n_levels;
+}
 
 gsq_status validate_config(const gsq_config* c) {
   if (!c) return fail(GSQ_EINVAL, "config is NULL");
   if (c->batch < 1 || c->out_features < 1 || c->in_features < 1)
     return fail(GSQ_EINVAL, "batch, out_features and in_features must be >= 1");
-  if (c->n_levels < 2 || c->n_levels > GSQ_MAX_LEVELS)
-    return fail(GSQ_EINVAL, "n_levels must be in [2, 8], got %d", c->n_levels);
+  if (c->relaxation != GSQ_RELAX_GRID && c->relaxation != GSQ_RELAX_SHIFT &&
+      c->relaxation != GSQ_RELAX_TERNARY)
+    return fail(GSQ_EINVAL, "unknown relaxation %d", c->relaxation);
+  const int nmax = c->relaxation == GSQ_RELAX_SHIFT ? GSQ_MAX_LEVELS : 8;
+  if (c->n_levels < 2 || c->n_levels > nmax)
+    return fail(GSQ_EINVAL, "n_levels must be in [2, %d] for this relaxation, got %d", nmax,
+                c->n_levels);
+  if (c->relaxation == GSQ_RELAX_TERNARY &&
+      !(c->n_levels == 3 && c->levels[0] == -1.f && c->levels[1] == 0.f && c->levels[2] == 1.f))
+    return fail(GSQ_EINVAL, "TERNARY needs the levels {-1, 0, 1}");
   float cmax = 0.f;
   for (int k = 0; k < c->n_levels; ++k) {
     if (!std::isfinite(c->levels[k])) return fail(GSQ_EINVAL, "level %d is not finite", k);
@@ -52,13 +65,16 @@ gsq_status validate_config(const gsq_config* c) {
     cmax = std::fmax(cmax, std::fabs(c->levels[k]));
   }
   if (cmax == 0.f) return fail(GSQ_EINVAL, "levels are all zero");
-  if (c->layout == GSQ_LAYOUT_GROUP) {
+  if (c->layout == GSQ_LAYOUT_GROUP || c->layout == GSQ_LAYOUT_BASE3) {
+    if (c->layout == GSQ_LAYOUT_BASE3 && c->n_levels != 3)
+      return fail(GSQ_EINVAL, "BASE3 stores 3-level codes, got n_levels %d", c->n_levels);
     const int gs = c->group_size;
     if (gs != 16 && gs != 32 && gs != 64 && gs != 128 && gs != 256)
       return fail(GSQ_EINVAL, "group_size must be 16, 32, 64, 128 or 256, got %d", gs);
     if (c->in_features % gs) return fail(GSQ_EINVAL, "in_features must be a multiple of group_size");
   } else if (c->layout == GSQ_LAYOUT_SUPERBLOCK) {
     if (c->in_features % 256) return fail(GSQ_EINVAL, "SUPERBLOCK needs in_features % 256 == 0");
+    if (c->n_levels > 8) return fail(GSQ_EINVAL, "SUPERBLOCK stores 3-bit codes (n_levels <= 8)");
   } else {
     return fail(GSQ_EINVAL, "unknown layout %d", c->layout);
   }
@@ -80,7 +96,7 @@ void free_layer(gsq::Layer* L) {
   }
   for (hipEvent_t e : L->event_pool) (void)hipEventDestroy(e);
   void* bufs[] = {L->W, L->H, L->L, L->M, L->V, L->S, L->MS, L->VS, L->R[0], L->R[1],
-                  L->G, L->partials, L->flag, L->sb_d, L->sb_sc, L->codes};
+                  L->G, L->partials, L->flag, L->sb_d, L->sb_sc, L->codes, L->J0};
   for (void* p : bufs)
     if (p) (void)hipFree(p);
   delete L;
@@ -162,7 +178,9 @@ size_t gsq_packed_size(const gsq_config* cfg) {
   if (validate_config(cfg) != GSQ_OK) return 0;
   const int64_t n = (int64_t)cfg->batch * cfg->out_features * cfg->in_features;
   if (cfg->layout == GSQ_LAYOUT_SUPERBLOCK) return (size_t)(n / 256 * 110);
-  return (size_t)(n * code_bits(cfg->n_levels) / 8 + 2 * (n / cfg->group_size));
+  const int64_t scales = 2 * (n / cfg->group_size);
+  if (cfg->layout == GSQ_LAYOUT_BASE3) return (size_t)((n + 4) / 5 + scales);
+  return (size_t)(n * code_bits(cfg->n_levels) / 8 + scales);
 }
 
 gsq_status gsq_layer_init(const gsq_config* cfg, const void* W, int32_t w_dtype, const float* H,
@@ -181,7 +199,10 @@ gsq_status gsq_layer_init(const gsq_config* cfg, const void* W, int32_t w_dtype,
   if (!h) return fail(GSQ_ENOMEM, "host allocation failed");
   gsq::Layer& L = *h;
   L.cfg = *cfg;
-  L.B = cfg->batch; L.O = cfg->out_features; L.I = cfg->in_features; L.K = cfg->n_levels;
+  L.B = cfg->batch; L.O = cfg->out_features; L.I = cfg->in_features;
+  L.K = logits_per_coord(*cfg);
+  L.n_grid = cfg->n_levels;
+  L.relax = cfg->relaxation;
   L.gs = cfg->layout == GSQ_LAYOUT_SUPERBLOCK ? 16 : cfg->group_size;
   L.Opad = round_up(L.O, gsq::kTileM);
   L.Ipad = round_up(L.I, gsq::kPadK);
@@ -201,6 +222,7 @@ gsq_status gsq_layer_init(const gsq_config* cfg, const void* W, int32_t w_dtype,
             alloc(&L.flag, sizeof(int)) && alloc(&L.codes, (size_t)L.N);
   if (ok && cfg->layout == GSQ_LAYOUT_SUPERBLOCK)
     ok = alloc(&L.sb_d, (L.N / 256) * 2) && alloc(&L.sb_sc, L.N / 16);
+  if (ok && cfg->relaxation == GSQ_RELAX_SHIFT) ok = alloc(&L.J0, (size_t)L.N);
   if (!ok) {
     free_layer(h);
     return fail(GSQ_ENOMEM, "device allocation failed for a %lld x %lld x %lld layer",
@@ -217,10 +239,10 @@ gsq_status gsq_layer_init(const gsq_config* cfg, const void* W, int32_t w_dtype,
     GSQ_HIP(hipMemsetAsync(L.VS, 0, L.NG * 4, stream));
     GSQ_HIP(hipMemsetAsync(L.flag, 0, sizeof(int), stream));
     float cmax = 0.f;
-    for (int k = 0; k < L.K; ++k) cmax = std::fmax(cmax, std::fabs(cfg->levels[k]));
+    for (int k = 0; k < L.n_grid; ++k) cmax = std::fmax(cmax, std::fabs(cfg->levels[k]));
     GSQ_HIP(timed(L, GSQ_KERNEL_INIT, stream, [&] { return gsq::launch_init_scales(L, scales_init, cmax, stream); }));
-    double mids[8] = {0};
-    for (int k = 0; k + 1 < L.K; ++k)
+    double mids[GSQ_MAX_LEVELS] = {0};
+    for (int k = 0; k + 1 < L.n_grid; ++k)
       mids[k] = 0.5 * ((double)cfg->levels[k] + (double)cfg->levels[k + 1]);
     GSQ_HIP(timed(L, GSQ_KERNEL_INIT, stream, [&] { return gsq::launch_init_logits(L, mids, stream); }));
     return GSQ_OK;
@@ -392,10 +414,12 @@ gsq_status gsq_pack(gsq_layer* h, void* packed, size_t packed_bytes, hipStream_t
 }
 
 gsq_status gsq_get_state(gsq_layer* h, float* logits, float* m, float* v, float* scales, float* m_s,
-                         float* v_s, int64_t* t, hipStream_t stream) {
+                         float* v_s, uint8_t* base, int64_t* t, hipStream_t stream) {
   g_err.clear();
   if (!h) return fail(GSQ_EINVAL, "handle is NULL");
   gsq::Layer& L = *h;
+  if (base && !L.J0) return fail(GSQ_EINVAL, "base indices exist only for the SHIFT relaxation");
+  if (base) GSQ_HIP(hipMemcpyAsync(base, L.J0, (size_t)L.N, hipMemcpyDeviceToDevice, stream));
   if (logits) GSQ_HIP(gsq::launch_state_io(L, logits, L.L, false, stream));
   if (m) GSQ_HIP(gsq::launch_state_io(L, m, L.M, false, stream));
   if (v) GSQ_HIP(gsq::launch_state_io(L, v, L.V, false, stream));
@@ -408,12 +432,14 @@ gsq_status gsq_get_state(gsq_layer* h, float* logits, float* m, float* v, float*
 }
 
 gsq_status gsq_set_state(gsq_layer* h, const float* logits, const float* m, const float* v,
-                         const float* scales, const float* m_s, const float* v_s, int64_t t,
-                         hipStream_t stream) {
+                         const float* scales, const float* m_s, const float* v_s,
+                         const uint8_t* base, int64_t t, hipStream_t stream) {
   g_err.clear();
   if (!h) return fail(GSQ_EINVAL, "handle is NULL");
   if (t < 0 || t >= (int64_t)UINT32_MAX) return fail(GSQ_EINVAL, "t out of range");
   gsq::Layer& L = *h;
+  if (base && !L.J0) return fail(GSQ_EINVAL, "base indices exist only for the SHIFT relaxation");
+  if (base) GSQ_HIP(hipMemcpyAsync(L.J0, base, (size_t)L.N, hipMemcpyDeviceToDevice, stream));
   if (scales && L.cfg.layout == GSQ_LAYOUT_SUPERBLOCK)
     return fail(GSQ_EUNSUPPORTED, "SUPERBLOCK scales are fixed by their 6-bit encoding");
   if (logits) GSQ_HIP(gsq::launch_state_io(L, const_cast<float*>(logits), L.L, true, stream));

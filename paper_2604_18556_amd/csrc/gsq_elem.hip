@@ -70,9 +70,9 @@ __device__ __forceinline__ float fast_sqrt(float x) { return __builtin_amdgcn_sq
 // One coordinate's relaxed sample (Alg. 1): p = softmax((kappa l + g) / tau), with the
 // largest perturbed logit r subtracted first.  vp = sum_k p_k (c_k - c_r), so that the soft
 // level v = c_r + vp and c_k - v = (c_k - c_r) - vp keep full relative accuracy when one
-// level holds almost all the mass.
+// level holds almost all the mass.  c holds the values the K logits stand for.
 template <int K, bool kF64>
-__device__ __forceinline__ void soft_sample(const float (&l)[K], const float (&c)[8], const float (&g)[K],
+__device__ __forceinline__ void soft_sample(const float (&l)[K], const float (&c)[K], const float (&g)[K],
                                             float kappa, Real<kF64> inv_tau, Real<kF64> (&p)[K],
                                             Real<kF64>& vp, Real<kF64>& cr) {
   using T = Real<kF64>;
@@ -101,24 +101,124 @@ __device__ __forceinline__ void soft_sample(const float (&l)[K], const float (&c
   for (int k = 0; k < K; ++k) { p[k] *= rz; vp += p[k] * ((T)c[k] - cr); }
 }
 
-// Noise of the thread's chunk of four coordinates (or zeros when sampling is off).
-template <int K, bool kF64>
-__device__ __forceinline__ void chunk_noise(float (&g)[4][K], const ElemArgs& a, uint64_t e0,
-                                            uint32_t t, uint32_t sample) {
-  if (a.noise) {
-    draw_chunk<K, kF64>(g, a.seed, e0, t, sample);
+// Two-value relaxation with logits {-l, l} (§3): p1 = softmax over (-kappa l + g0,
+// kappa l + g1) / tau, i.e. a sigmoid of (2 kappa l + g1 - g0) / tau.  The smaller
+// probability is formed as e / (1 + e) with e = exp(-|a|), never as 1 - p.
+template <bool kF64>
+__device__ __forceinline__ void pair_probs(float l, float g0, float g1, float kappa, Real<kF64> inv_tau,
+                                           Real<kF64>& p0, Real<kF64>& p1) {
+  using T = Real<kF64>;
+  const T d = (T)2 * (T)kappa * (T)l + ((T)g1 - (T)g0);
+  const T a = d * inv_tau;
+  T e, big;
+  if constexpr (kF64) {
+    e = exp(-fabs(a));
+    big = T(1) / (T(1) + e);
+  } else {
+    e = __builtin_amdgcn_exp2f(-fabsf(a) * kLog2e);
+    big = fast_rcp(1.f + e);
+  }
+  const T small = e * big;
+  p1 = a >= T(0) ? big : small;
+  p0 = a >= T(0) ? small : big;
+}
+
+// Gumbel values per coordinate and draw: one per logit, or the mask's two and the sign's two.
+template <int K, int kMode>
+constexpr int noise_count() { return kMode == GSQ_RELAX_TERNARY ? 4 : K; }
+
+// One coordinate's relaxed sample in any relaxation: the soft level v (W_hat = s v) and
+// jac[k] = (tau / kappa) dv/dl_k.
+//   GRID / SHIFT: v = sum_k p_k c_k, jac[k] = p_k (c_k - v).
+//   TERNARY: v = m~ b~ with m~ = p1 of the mask pair (values 0, 1) and b~ = p1 - p0 of the
+//   sign pair (values -1, 1); a pair with logits {-l, l} and values (y0, y1) has
+//   (tau / kappa) dy/dl = 2 p0 p1 (y1 - y0), so jac = (2 p0 p1 b~, 4 p0 p1 m~).
+template <int K, int Z, bool kF64, int kMode>
+__device__ __forceinline__ void coord_sample(const float (&l)[K], const float (&c)[K], const float (&g)[Z],
+                                             float kappa, Real<kF64> inv_tau, Real<kF64>& v,
+                                             Real<kF64> (&jac)[K]) {
+  using T = Real<kF64>;
+  if constexpr (kMode == GSQ_RELAX_TERNARY) {
+    static_assert(K == 2 && Z == 4, "ternary: two logits, four noise values");
+    T pm0, pm1, pb0, pb1;
+    pair_probs<kF64>(l[0], g[0], g[1], kappa, inv_tau, pm0, pm1);
+    pair_probs<kF64>(l[1], g[2], g[3], kappa, inv_tau, pb0, pb1);
+    const T m = pm1, b = pb1 - pb0;
+    v = m * b;
+    jac[0] = b * (T(2) * pm0 * pm1);
+    jac[1] = m * (T(4) * pb0 * pb1);
+  } else {
+    static_assert(K == Z, "one noise value per logit");
+    T p[K], vp, cr;
+    soft_sample<K, kF64>(l, c, g, kappa, inv_tau, p, vp, cr);
+    v = cr + vp;
+#pragma unroll
+    for (int k = 0; k < K; ++k) jac[k] = p[k] * (((T)c[k] - cr) - vp);
+  }
+}
+
+// Local-shift windows in LDS: row j (a grid index) holds the levels of the five shifts around
+// it, c[clip(j + k - 2, 0, n - 1)] for k < 5, padded to 8 floats.  Rows past the grid are
+// filled like the last one, so a clamped index never reads an unset row.
+constexpr int kWinRow = 8;
+__device__ __forceinline__ void fill_windows(float* win, const ElemArgs& a) {
+  for (int i = threadIdx.x; i < GSQ_MAX_LEVELS * kWinRow; i += blockDim.x) {
+    const int j = i / kWinRow, k = i % kWinRow;
+    int idx = j + k - 2;
+    idx = idx < 0 ? 0 : idx;
+    idx = idx > a.n_grid - 1 ? a.n_grid - 1 : idx;
+    float v = 0.f;
+#pragma unroll
+    for (int m = 0; m < GSQ_MAX_LEVELS; ++m) v = (m == idx) ? a.c[m] : v;
+    win[i] = k < GSQ_SHIFT_WINDOW ? v : 0.f;
+  }
+  __syncthreads();
+}
+
+// The values the logits of the chunk's four coordinates stand for.
+template <int K, int kMode>
+__device__ __forceinline__ void chunk_candidates(float (&cand)[4][K], const ElemArgs& a, const float* win,
+                                                 int64_t e0) {
+  if constexpr (kMode == GSQ_RELAX_SHIFT) {
+    static_assert(K == GSQ_SHIFT_WINDOW, "five shifts");
+    const uint32_t j4 = *reinterpret_cast<const uint32_t*>(a.J0 + e0);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      int j = (int)((j4 >> (8 * q)) & 0xFFu);
+      j = j < a.n_grid ? j : a.n_grid - 1;          // a corrupt index cannot leave the table
+      const float4 lo = *reinterpret_cast<const float4*>(win + j * kWinRow);
+      cand[q][0] = lo.x; cand[q][1] = lo.y; cand[q][2] = lo.z; cand[q][3] = lo.w;
+      cand[q][4] = win[j * kWinRow + 4];
+    }
   } else {
 #pragma unroll
     for (int q = 0; q < 4; ++q)
 #pragma unroll
-      for (int k = 0; k < K; ++k) g[q][k] = 0.f;
+      for (int k = 0; k < K; ++k) cand[q][k] = a.c[k];
+  }
+}
+
+// Noise of the thread's chunk of four coordinates (or zeros when sampling is off).
+template <int Z, bool kF64>
+__device__ __forceinline__ void chunk_noise(float (&g)[4][Z], const ElemArgs& a, uint64_t e0,
+                                            uint32_t t, uint32_t sample) {
+  if (a.noise) {
+    draw_chunk<Z, kF64>(g, a.seed, e0, t, sample);
+  } else {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int k = 0; k < Z; ++k) g[q][k] = 0.f;
   }
 }
 
 // ------------------------------------------------------------------ forward: R = W - s * v
-template <int K, bool kF64>
+template <int K, bool kF64, int kMode>
 __global__ __launch_bounds__(kBlock) void k_forward(ElemArgs a) {
   using T = Real<kF64>;
+  constexpr int Z = noise_count<K, kMode>();
+  __shared__ __align__(16) float win[kMode == GSQ_RELAX_SHIFT ? GSQ_MAX_LEVELS * kWinRow : 4];
+  if constexpr (kMode == GSQ_RELAX_SHIFT) fill_windows(win, a);
   const int lane = threadIdx.x & 63;
   const int64_t col0 = (int64_t)blockIdx.x * kCols + lane * 4;
   const T inv_tau = kF64 ? (T)a.inv_tau_d : (T)a.inv_tau;
@@ -133,17 +233,19 @@ __global__ __launch_bounds__(kBlock) void k_forward(ElemArgs a) {
     float4 lv[K];
 #pragma unroll
     for (int k = 0; k < K; ++k) lv[k] = *reinterpret_cast<const float4*>(a.L + k * a.N + e0);
-    float g[4][K];
-    chunk_noise<K, kF64>(g, a, (uint64_t)e0, a.t, (uint32_t)a.sample);
+    float cand[4][K];
+    chunk_candidates<K, kMode>(cand, a, win, e0);
+    float g[4][Z];
+    chunk_noise<Z, kF64>(g, a, (uint64_t)e0, a.t, (uint32_t)a.sample);
     float r[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       float l[K];
 #pragma unroll
       for (int k = 0; k < K; ++k) l[k] = f4get(lv[k], q);
-      T p[K], vp, cr;
-      soft_sample<K, kF64>(l, a.c, g[q], a.kappa, inv_tau, p, vp, cr);
-      r[q] = (float)((T)w[q] - s * (cr + vp));
+      T v, jac[K];
+      coord_sample<K, Z, kF64, kMode>(l, cand[q], g[q], a.kappa, inv_tau, v, jac);
+      r[q] = (float)((T)w[q] - s * v);
     }
     store_r4<kF64>(a.Rout, padded_index(a, row, col0), r);
   }
@@ -176,9 +278,12 @@ __device__ __forceinline__ void opt_update(bool lion, Real<kF64> d, Real<kF64>& 
 // dL/dl_k = (kappa / tau) G s p_k (c_k - v); dL/ds = sum over the group of G v.  Adam (bias
 // correction at step n = t + 1) or Lion.  With a.fuse, the sample of step t + 1 is drawn from
 // the updated logits and scale and its residual written to a.Rout.
-template <int K, bool kF64, bool kScales, bool kMulti>
+template <int K, bool kF64, bool kScales, bool kMulti, int kMode>
 __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
   using T = Real<kF64>;
+  constexpr int Z = noise_count<K, kMode>();
+  __shared__ __align__(16) float win[kMode == GSQ_RELAX_SHIFT ? GSQ_MAX_LEVELS * kWinRow : 4];
+  if constexpr (kMode == GSQ_RELAX_SHIFT) fill_windows(win, a);
   const int lane = threadIdx.x & 63;
   const int64_t col0 = (int64_t)blockIdx.x * kCols + lane * 4;
   const bool active = col0 < a.I;
@@ -213,6 +318,8 @@ __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
 #pragma unroll
       for (int k = 0; k < K; ++k) lv[k] = mv[k] = vv[k] = make_float4(0.f, 0.f, 0.f, 0.f);
     }
+    float cand[4][K];
+    chunk_candidates<K, kMode>(cand, a, win, e0);
     // gradient, averaged over the step's independent samples (one unless kMulti)
     T ds_part = 0;
     T dacc[4][K];
@@ -224,20 +331,20 @@ __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
     for (int smp = 0; smp < M; ++smp) {
       const float4 gv = active ? *reinterpret_cast<const float4*>(a.G + smp * a.g_stride + gidx)
                                : make_float4(0.f, 0.f, 0.f, 0.f);
-      float g[4][K];
-      chunk_noise<K, kF64>(g, a, (uint64_t)e0, a.t, (uint32_t)smp);
+      float g[4][Z];
+      chunk_noise<Z, kF64>(g, a, (uint64_t)e0, a.t, (uint32_t)smp);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         float l[K];
 #pragma unroll
         for (int k = 0; k < K; ++k) l[k] = f4get(lv[k], q);
-        T p[K], vp, cr;
-        soft_sample<K, kF64>(l, a.c, g[q], a.kappa, inv_tau, p, vp, cr);
+        T v, jac[K];
+        coord_sample<K, Z, kF64, kMode>(l, cand[q], g[q], a.kappa, inv_tau, v, jac);
         const T gq = (T)f4get(gv, q);
-        ds_part += gq * (cr + vp);
+        ds_part += gq * v;
         const T coef = kt * (gq * s);
 #pragma unroll
-        for (int k = 0; k < K; ++k) dacc[q][k] += coef * p[k] * (((T)a.c[k] - cr) - vp);
+        for (int k = 0; k < K; ++k) dacc[q][k] += coef * jac[k];
       }
     }
     if constexpr (kMulti) {
@@ -292,17 +399,17 @@ __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
       const T inv_tau_n = kF64 ? (T)a.inv_tau_n_d : (T)a.inv_tau_n;
       float w[4];
       load_w4(a.W, a.w_bf16, e0, w);
-      float g[4][K];
-      chunk_noise<K, kF64>(g, a, (uint64_t)e0, a.t_next, 0u);
+      float g[4][Z];
+      chunk_noise<Z, kF64>(g, a, (uint64_t)e0, a.t_next, 0u);
       float r[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         float l[K];
 #pragma unroll
         for (int k = 0; k < K; ++k) l[k] = f4get(lv[k], q);
-        T p[K], vp, cr;
-        soft_sample<K, kF64>(l, a.c, g[q], a.kappa_n, inv_tau_n, p, vp, cr);
-        r[q] = (float)((T)w[q] - (T)s_new * (cr + vp));
+        T v, jac[K];
+        coord_sample<K, Z, kF64, kMode>(l, cand[q], g[q], a.kappa_n, inv_tau_n, v, jac);
+        r[q] = (float)((T)w[q] - (T)s_new * v);
       }
       store_r4<kF64>(a.Rout, padded_index(a, row, col0), r);
     }
@@ -375,35 +482,47 @@ __global__ void k_init_scales_superblock(const void* W, int w_bf16, float* S, ui
 }
 
 struct InitConsts {
-  float c[8];
-  double mids[8];   // (c_k + c_{k+1}) / 2, exact in fp64
-  int K;
+  float c[GSQ_MAX_LEVELS];
+  double mids[GSQ_MAX_LEVELS];   // (c_k + c_{k+1}) / 2, exact in fp64
+  int K;                         // logits per coordinate
+  int n_grid;
+  int relax;
   float alpha, sigma;
   int noise;
   uint64_t seed;
 };
 
-// Round-to-nearest code (fp32 ratio, ties to the lower level), then the Gaussian prior of
-// App. A around it, mean-subtracted, plus Eq. 4's N(0,1) noise (Box-Muller on Philox stream 1):
-// l = sigma_init * (eps + alpha * prior).  fp64 arithmetic, fp32 storage.
-__global__ void k_init_logits(const void* W, int w_bf16, const float* S, float* L, int64_t N,
-                              int gs, InitConsts ic) {
+// Round-to-nearest code q (fp32 ratio, ties to the lower level), then the warm-start logits
+// around it plus Eq. 4's N(0,1) noise (Box-Muller on Philox stream 1):
+// l = sigma_init * (eps + alpha * prior).
+//   GRID: prior_k = -(c_k - c_q)^2 / 2, mean-subtracted (App. A);
+//   SHIFT: j0 = q and prior_k = -delta_k^2 / 2, mean-subtracted (App. A, b > 2);
+//   TERNARY: Eq. 3, prior = (q != 0 ? 1 : -1, sign of q) for the level c_q in {-1, 0, 1}.
+// fp64 arithmetic, fp32 storage.
+__global__ void k_init_logits(const void* W, int w_bf16, const float* S, float* L, uint8_t* J0,
+                              int64_t N, int gs, InitConsts ic) {
   for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < N;
        e += (int64_t)gridDim.x * blockDim.x) {
     const float w = load_w1(W, w_bf16, e);
     const float s = S[e / gs];
     const float u = s != 0.f ? __fdiv_rn(w, s) : 0.f;
     int q = 0;
-    for (int k = 0; k + 1 < ic.K; ++k) q += ((double)u > ic.mids[k]) ? 1 : 0;
-    double cq = 0.0;
-    for (int k = 0; k < ic.K; ++k) if (k == q) cq = (double)ic.c[k];
+    for (int k = 0; k + 1 < ic.n_grid; ++k) q += ((double)u > ic.mids[k]) ? 1 : 0;
     double mu[8], mean = 0.0;
-    for (int k = 0; k < ic.K; ++k) {
-      const double dlt = (double)ic.c[k] - cq;
-      mu[k] = -0.5 * dlt * dlt;
-      mean += mu[k];
+    if (ic.relax == GSQ_RELAX_TERNARY) {
+      mu[0] = q != 1 ? 1.0 : -1.0;
+      mu[1] = (double)(q - 1);
+    } else {
+      double cq = 0.0;
+      for (int k = 0; k < ic.n_grid; ++k) if (k == q) cq = (double)ic.c[k];
+      for (int k = 0; k < ic.K; ++k) {
+        const double dlt = ic.relax == GSQ_RELAX_SHIFT ? (double)(k - 2) : (double)ic.c[k] - cq;
+        mu[k] = -0.5 * dlt * dlt;
+        mean += mu[k];
+      }
+      mean /= (double)ic.K;
+      if (ic.relax == GSQ_RELAX_SHIFT) J0[e] = (uint8_t)q;
     }
-    mean /= (double)ic.K;
     float eps[8];
     for (int k = 0; k < 8; ++k) eps[k] = 0.f;
     if (ic.noise) {
@@ -425,24 +544,38 @@ __global__ void k_init_logits(const void* W, int w_bf16, const float* S, float* 
 }
 
 // ------------------------------------------------------------------ hardening and packing
-// Codes q = argmax_k l_k (ties to the lowest k); optionally the hard residual R = W - s c[q]
-// (s rounded to fp16 in the group layout) written in the contraction's padded layout,
-// fp32 when r_f32 != 0, bf16 otherwise.
-__global__ void k_harden(ElemArgs a, int K, int superblock, int r_f32, uint8_t* codes, void* Rh) {
+// Grid codes: GRID: q = argmax_k l_k (ties to the lowest k); SHIFT: clip(j0 + delta*) with
+// delta* the argmax shift; TERNARY: Alg. 2's thresholds, active iff l_m >= 0, positive iff
+// l_b >= 0, q = 1 + mask * sign.  Optionally the hard residual R = W - s c[q] (s rounded to
+// fp16 in the group layouts) written in the contraction's padded layout, fp32 when
+// r_f32 != 0, bf16 otherwise.
+__global__ void k_harden(ElemArgs a, int K, int relax, int superblock, int r_f32, uint8_t* codes,
+                         void* Rh) {
   for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < a.N;
        e += (int64_t)gridDim.x * blockDim.x) {
-    float best = a.L[e];
     int q = 0;
-    for (int k = 1; k < K; ++k) {
-      const float x = a.L[k * a.N + e];
-      if (x > best) { best = x; q = k; }
+    if (relax == GSQ_RELAX_TERNARY) {
+      const bool active = a.L[e] >= 0.f, positive = a.L[a.N + e] >= 0.f;
+      q = active ? (positive ? 2 : 0) : 1;
+    } else {
+      float best = a.L[e];
+      for (int k = 1; k < K; ++k) {
+        const float x = a.L[k * a.N + e];
+        if (x > best) { best = x; q = k; }
+      }
+      if (relax == GSQ_RELAX_SHIFT) {
+        int j = a.J0[e];
+        j = j < a.n_grid ? j : a.n_grid - 1;
+        q = j + q - 2;
+        q = q < 0 ? 0 : (q > a.n_grid - 1 ? a.n_grid - 1 : q);
+      }
     }
     if (codes) codes[e] = (uint8_t)q;
     if (Rh) {
       float s = a.S[e / a.gs];
       if (!superblock) s = __half2float(__float2half_rn(s));
       float cq = a.c[0];
-      for (int k = 1; k < K; ++k) if (k == q) cq = a.c[k];
+      for (int k = 1; k < GSQ_MAX_LEVELS; ++k) if (k == q) cq = a.c[k];
       const float r = load_w1(a.W, a.w_bf16, e) - s * cq;
       const int64_t row = e / a.I;
       const int64_t idx = padded_index(a, row, e - row * a.I);
@@ -475,6 +608,20 @@ __global__ void k_pack_codes(const uint8_t* codes, uint8_t* out, int64_t n8, int
       word |= code << (b * q);
     }
     for (int by = 0; by < b; ++by) out[j * b + by] = (uint8_t)(word >> (8 * by));
+  }
+}
+
+// Base-3 layout, code section: five consecutive codes t_j -> one byte sum_j t_j 3^j (codes past
+// the end count as 0).
+__global__ void k_pack_base3(const uint8_t* codes, uint8_t* out, int64_t n, int64_t nbytes) {
+  for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < nbytes;
+       j += (int64_t)gridDim.x * blockDim.x) {
+    uint32_t byte = 0;
+    for (int i = 4; i >= 0; --i) {
+      const int64_t idx = 5 * j + i;
+      byte = 3u * byte + (idx < n ? (uint32_t)codes[idx] : 0u);
+    }
+    out[j] = (uint8_t)byte;
   }
 }
 
@@ -581,7 +728,9 @@ ElemArgs base_args(const Layer& L) {
   a.gs = (int32_t)L.gs;
   a.w_bf16 = L.w_bf16;
   a.seed = L.cfg.seed;
-  for (int k = 0; k < 8; ++k) a.c[k] = k < L.K ? L.cfg.levels[k] : 0.f;
+  a.J0 = L.J0;
+  a.n_grid = L.n_grid;
+  for (int k = 0; k < GSQ_MAX_LEVELS; ++k) a.c[k] = k < L.n_grid ? L.cfg.levels[k] : 0.f;
   return a;
 }
 
@@ -608,28 +757,32 @@ hipError_t launch_init_scales(const Layer& L, const float* scales_init, float cm
 
 hipError_t launch_init_logits(const Layer& L, const double* mids, hipStream_t s) {
   InitConsts ic{};
-  for (int k = 0; k < 8; ++k) {
-    ic.c[k] = k < L.K ? L.cfg.levels[k] : 0.f;
-    ic.mids[k] = k + 1 < L.K ? mids[k] : 0.0;
+  for (int k = 0; k < GSQ_MAX_LEVELS; ++k) {
+    ic.c[k] = k < L.n_grid ? L.cfg.levels[k] : 0.f;
+    ic.mids[k] = k + 1 < L.n_grid ? mids[k] : 0.0;
   }
   ic.K = (int)L.K;
+  ic.n_grid = L.n_grid;
+  ic.relax = L.relax;
   ic.alpha = L.cfg.alpha;
   ic.sigma = L.cfg.sigma_init;
   ic.noise = L.cfg.init_noise;
   ic.seed = L.cfg.seed;
-  hipLaunchKernelGGL(k_init_logits, flat_grid(L.N), dim3(256), 0, s, L.W, L.w_bf16, L.S, L.L, L.N,
-                     (int)L.gs, ic);
+  hipLaunchKernelGGL(k_init_logits, flat_grid(L.N), dim3(256), 0, s, L.W, L.w_bf16, L.S, L.L, L.J0,
+                     L.N, (int)L.gs, ic);
   return hipGetLastError();
 }
 
-template <int K>
+template <int K, int kMode = GSQ_RELAX_GRID>
 static hipError_t forward_k(const Layer& L, const ElemArgs& a, hipStream_t s) {
-  if (L.bf16) hipLaunchKernelGGL((k_forward<K, false>), row_grid(L), dim3(kBlock), 0, s, a);
-  else hipLaunchKernelGGL((k_forward<K, true>), row_grid(L), dim3(kBlock), 0, s, a);
+  if (L.bf16) hipLaunchKernelGGL((k_forward<K, false, kMode>), row_grid(L), dim3(kBlock), 0, s, a);
+  else hipLaunchKernelGGL((k_forward<K, true, kMode>), row_grid(L), dim3(kBlock), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_forward(const Layer& L, const ElemArgs& a, hipStream_t s) {
+  if (L.relax == GSQ_RELAX_SHIFT) return forward_k<GSQ_SHIFT_WINDOW, GSQ_RELAX_SHIFT>(L, a, s);
+  if (L.relax == GSQ_RELAX_TERNARY) return forward_k<2, GSQ_RELAX_TERNARY>(L, a, s);
   switch (L.K) {
     case 2: return forward_k<2>(L, a, s);
     case 3: return forward_k<3>(L, a, s);
@@ -641,26 +794,29 @@ hipError_t launch_forward(const Layer& L, const ElemArgs& a, hipStream_t s) {
   }
 }
 
-template <int K, bool kMulti>
+template <int K, bool kMulti, int kMode>
 static void backward_km(const Layer& L, const ElemArgs& a, bool sc, hipStream_t s) {
   const dim3 g = row_grid(L), b(kBlock);
   if (L.bf16) {
-    if (sc) hipLaunchKernelGGL((k_backward<K, false, true, kMulti>), g, b, 0, s, a);
-    else hipLaunchKernelGGL((k_backward<K, false, false, kMulti>), g, b, 0, s, a);
+    if (sc) hipLaunchKernelGGL((k_backward<K, false, true, kMulti, kMode>), g, b, 0, s, a);
+    else hipLaunchKernelGGL((k_backward<K, false, false, kMulti, kMode>), g, b, 0, s, a);
   } else {
-    if (sc) hipLaunchKernelGGL((k_backward<K, true, true, kMulti>), g, b, 0, s, a);
-    else hipLaunchKernelGGL((k_backward<K, true, false, kMulti>), g, b, 0, s, a);
+    if (sc) hipLaunchKernelGGL((k_backward<K, true, true, kMulti, kMode>), g, b, 0, s, a);
+    else hipLaunchKernelGGL((k_backward<K, true, false, kMulti, kMode>), g, b, 0, s, a);
   }
 }
 
-template <int K>
+template <int K, int kMode = GSQ_RELAX_GRID>
 static hipError_t backward_k(const Layer& L, const ElemArgs& a, bool sc, hipStream_t s) {
-  if (a.samples > 1) backward_km<K, true>(L, a, sc, s);
-  else backward_km<K, false>(L, a, sc, s);
+  if (a.samples > 1) backward_km<K, true, kMode>(L, a, sc, s);
+  else backward_km<K, false, kMode>(L, a, sc, s);
   return hipGetLastError();
 }
 
 hipError_t launch_backward(const Layer& L, const ElemArgs& a, bool update_scales, hipStream_t s) {
+  if (L.relax == GSQ_RELAX_SHIFT)
+    return backward_k<GSQ_SHIFT_WINDOW, GSQ_RELAX_SHIFT>(L, a, update_scales, s);
+  if (L.relax == GSQ_RELAX_TERNARY) return backward_k<2, GSQ_RELAX_TERNARY>(L, a, update_scales, s);
   switch (L.K) {
     case 2: return backward_k<2>(L, a, update_scales, s);
     case 3: return backward_k<3>(L, a, update_scales, s);
@@ -674,7 +830,7 @@ hipError_t launch_backward(const Layer& L, const ElemArgs& a, bool update_scales
 
 hipError_t launch_harden(const Layer& L, uint8_t* codes, void* Rh, hipStream_t s) {
   const ElemArgs a = base_args(L);
-  hipLaunchKernelGGL(k_harden, flat_grid(L.N), dim3(256), 0, s, a, (int)L.K,
+  hipLaunchKernelGGL(k_harden, flat_grid(L.N), dim3(256), 0, s, a, (int)L.K, L.relax,
                      L.cfg.layout == GSQ_LAYOUT_SUPERBLOCK ? 1 : 0, L.bf16 ? 0 : 1, codes, Rh);
   return hipGetLastError();
 }
@@ -692,12 +848,20 @@ hipError_t launch_pack(const Layer& L, const uint8_t* codes, uint8_t* out, hipSt
                        out, nrec);
     return hipGetLastError();
   }
-  const int b = L.K <= 2 ? 1 : L.K <= 4 ? 2 : 3;
-  const int64_t n8 = L.N / 8;
-  hipLaunchKernelGGL(k_pack_codes, flat_grid(n8), dim3(256), 0, s, codes, out, n8, b);
+  int64_t code_bytes;
+  if (L.cfg.layout == GSQ_LAYOUT_BASE3) {
+    code_bytes = (L.N + 4) / 5;
+    hipLaunchKernelGGL(k_pack_base3, flat_grid(code_bytes), dim3(256), 0, s, codes, out, L.N,
+                       code_bytes);
+  } else {
+    const int b = L.n_grid <= 2 ? 1 : L.n_grid <= 4 ? 2 : L.n_grid <= 8 ? 3 : 4;
+    const int64_t n8 = L.N / 8;
+    code_bytes = L.N * b / 8;
+    hipLaunchKernelGGL(k_pack_codes, flat_grid(n8), dim3(256), 0, s, codes, out, n8, b);
+  }
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(k_pack_scales, flat_grid(L.NG), dim3(256), 0, s, L.S, out + L.N * b / 8, L.NG,
+  hipLaunchKernelGGL(k_pack_scales, flat_grid(L.NG), dim3(256), 0, s, L.S, out + code_bytes, L.NG,
                      L.flag);
   return hipGetLastError();
 }
@@ -736,7 +900,9 @@ static hipError_t gumbel_k(const gsq_config& cfg, int64_t e0, int64_t count, int
 
 hipError_t launch_gumbel(const gsq_config& cfg, int64_t e0, int64_t count, int64_t t, float* out,
                          hipStream_t s) {
-  switch (cfg.n_levels) {
+  const int z = cfg.relaxation == GSQ_RELAX_SHIFT ? GSQ_SHIFT_WINDOW
+                : cfg.relaxation == GSQ_RELAX_TERNARY ? 4 : cfg.n_levels;
+  switch (z) {
     case 2: return gumbel_k<2>(cfg, e0, count, t, out, s);
     case 3: return gumbel_k<3>(cfg, e0, count, t, out, s);
     case 4: return gumbel_k<4>(cfg, e0, count, t, out, s);

@@ -19,14 +19,16 @@ struct ElemArgs {
   const void* W;        // B*O*I, fp32 or bf16
   const float* G;       // B*Opad*Ipad fp32
   void* Rout;           // B*Opad*Ipad, fp32 (FP32 path) or bf16
-  float *L, *M, *V;     // K planes of N fp32 each
+  float *L, *M, *V;     // K planes of N fp32 each (K = logits per coordinate)
+  const uint8_t* J0;    // local shift: initial grid index of every coordinate (N bytes)
   float *S, *MS, *VS;   // one per scale group
   int* flag;            // sticky non-finite flag
   int64_t N;            // B*O*I
   int32_t rows;         // B*O
   int32_t O, I, Opad, Ipad, gs, w_bf16;
   uint64_t seed;
-  float c[8];
+  float c[GSQ_MAX_LEVELS];    // the grid
+  int32_t n_grid;
   // this step's sample(s)
   uint32_t t;
   int32_t noise;
@@ -48,7 +50,9 @@ struct ElemArgs {
 
 struct Layer {
   gsq_config cfg;
-  int64_t B, O, I, K, gs, Opad, Ipad, N, NG;
+  int64_t B, O, I, K, gs, Opad, Ipad, N, NG;   // K: logits per coordinate
+  int n_grid;                                   // grid levels (code values)
+  int relax;                                    // GSQ_RELAX_*
   bool bf16;        // precision == GSQ_PREC_BF16
   int w_bf16;
   void* W = nullptr;
@@ -65,6 +69,7 @@ struct Layer {
   uint16_t* sb_d = nullptr;
   uint8_t* sb_sc = nullptr;
   uint8_t* codes = nullptr;
+  uint8_t* J0 = nullptr;       // local shift: initial grid indices
   int64_t t = 0;
   int cur = 0;            // R buffer holding a prepared sample (when r_valid)
   bool r_valid = false;

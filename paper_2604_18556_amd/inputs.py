@@ -42,6 +42,7 @@ class Workload:
     x_dist: str                # "normal" | "student_t4"
     outliers: bool
     lr_scales: float
+    relaxation: str = "grid"   # "grid" | "shift" | "ternary"
 
 
 WORKLOADS = {
@@ -58,6 +59,11 @@ WORKLOADS = {
                  8192, 300, "student_t4", True, 5e-5),
         Workload("moe-64x2048x7168-superblock", 5, 64, 2048, 7168, L8, 16, "superblock", "bf16",
                  2048, 200, "student_t4", True, 0.0),
+        # the same layers under the paper's other relaxations (same seeds, same data)
+        Workload("mlp-down-4096x14336-shift8", 3, 1, 4096, 14336, L8, 128, "group", "bf16",
+                 8192, 500, "student_t4", True, 5e-5, "shift"),
+        Workload("attn-4096x4096-ternary", 1, 1, 4096, 4096, L3, 128, "base3", "bf16",
+                 4096, 500, "student_t4", True, 5e-5, "ternary"),
     )
 }
 

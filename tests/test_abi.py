@@ -47,8 +47,9 @@ def test_ctypes_structs_match_the_c_layout(tmp_path):
 #include <stddef.h>
 #include "gsq.h"
 int main(void) {
-  printf("%zu %zu %zu %zu %zu\n", sizeof(gsq_config), offsetof(gsq_config, seed),
-         offsetof(gsq_config, init_noise), sizeof(gsq_step_params), offsetof(gsq_step_params, kappa_next));
+  printf("%zu %zu %zu %zu %zu %zu %zu\n", sizeof(gsq_config), offsetof(gsq_config, seed),
+         offsetof(gsq_config, init_noise), offsetof(gsq_config, relaxation), sizeof(gsq_step_params),
+         offsetof(gsq_step_params, kappa_next), offsetof(gsq_step_params, samples));
   return 0;
 }
 ''')
@@ -59,7 +60,8 @@ int main(void) {
         pytest.skip("cannot compile against hip_runtime_api.h: " + r.stderr[-300:])
     vals = [int(x) for x in subprocess.run([str(exe)], capture_output=True, text=True).stdout.split()]
     assert vals == [ctypes.sizeof(B.CConfig), B.CConfig.seed.offset, B.CConfig.init_noise.offset,
-                    ctypes.sizeof(B.CStepParams), B.CStepParams.kappa_next.offset]
+                    B.CConfig.relaxation.offset, ctypes.sizeof(B.CStepParams),
+                    B.CStepParams.kappa_next.offset, B.CStepParams.samples.offset]
 
 
 def _cfg(**kw):
@@ -74,12 +76,25 @@ def test_packed_size_formula(lib):
     assert B.packed_size(_cfg(levels=tuple(range(8)))) == 8 * 256 * 3 // 8 + 2 * 8 * 2
     assert B.packed_size(_cfg(batch=3, layout=B.LAYOUT_SUPERBLOCK, levels=tuple(range(8)))) == 3 * 8 * 110
     assert B.packed_size(_cfg(group_size=100)) == 0
+    # local shift over a 16-level (4-bit) grid
+    assert B.packed_size(_cfg(levels=tuple(range(16)), relaxation=B.RELAX_SHIFT)) == 8 * 256 * 4 // 8 + 2 * 8 * 2
+    # base-3: five codes per byte, the last byte padded
+    assert B.packed_size(_cfg(levels=(-1.0, 0.0, 1.0), layout=B.LAYOUT_BASE3)) == -(-8 * 256 // 5) + 2 * 8 * 2
+    assert B.packed_size(_cfg(out_features=3, levels=(-1.0, 0.0, 1.0), layout=B.LAYOUT_BASE3,
+                              relaxation=B.RELAX_TERNARY)) == -(-3 * 256 // 5) + 2 * 3 * 2
 
 
 @pytest.mark.parametrize("bad", [
     dict(levels=(0.5, -0.5, 1.5, 2.5)),            # not increasing
     dict(levels=(1.0,)),                           # K < 2
-    dict(levels=tuple(range(9))),                  # K > 8 (the binding fills at most 8)
+    dict(levels=tuple(range(9))),                  # a full-grid categorical over more than 8
+    dict(levels=tuple(range(17)), relaxation=B.RELAX_SHIFT),   # more than 16 grid levels
+    dict(levels=tuple(range(16)), relaxation=B.RELAX_SHIFT, layout=B.LAYOUT_SUPERBLOCK),
+    dict(levels=(-1.0, 0.0, 2.0), relaxation=B.RELAX_TERNARY),
+    dict(levels=(-1.5, -0.5, 0.5, 1.5), relaxation=B.RELAX_TERNARY),
+    dict(levels=(-1.5, -0.5, 0.5, 1.5), layout=B.LAYOUT_BASE3),
+    dict(relaxation=7),
+    dict(layout=3),
     dict(levels=(0.0, 0.0)),                       # not increasing / all zero
     dict(group_size=48),
     dict(in_features=200),                         # not a multiple of the group size
@@ -94,7 +109,7 @@ def test_invalid_configs_are_rejected_before_any_device_work(lib, bad):
     if "levels" in bad:
         lv = bad["levels"]
         c.n_levels = len(lv)
-        for k, x in enumerate(lv[:8]):
+        for k, x in enumerate(lv[:B.MAX_LEVELS]):
             c.levels[k] = x
     h = ctypes.c_void_p()
     st = lib.gsq_layer_init(ctypes.byref(c), ctypes.c_void_p(16), 0, ctypes.c_void_p(16), None, None,

@@ -14,7 +14,8 @@ from oracle import philox
 from paper_2604_18556_amd import binding as B
 from paper_2604_18556_amd import inputs
 
-from gpu_common import Pair, assert_state_close, oracle_params, rel_err
+from gpu_common import Pair, assert_state_close, layer_inputs, oracle_params, rel_err
+from gpu_common import warm_state as _warm
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -29,19 +30,6 @@ def dev():
         pytest.skip("no GPU")
     B.load()
     return torch.device("cuda:0")
-
-
-def layer_inputs(O, I, batch=1, bf16=True, seed=0, tokens=None):
-    rng = np.random.default_rng(100 + seed)
-    W = rng.normal(0, 0.02, (batch, O, I)).astype(np.float32)
-    W.reshape(-1)[rng.choice(W.size, max(1, W.size // 1000), replace=False)] *= 10
-    if bf16:
-        W = inputs.to_bf16_values(W)
-    Hs = []
-    for b in range(batch):
-        X = rng.standard_t(4, (tokens or 2 * I, I)) * rng.lognormal(0, 0.5, I)
-        Hs.append((X.T @ X).astype(np.float32))
-    return W, np.stack(Hs)
 
 
 # ------------------------------------------------------------------ noise
@@ -104,17 +92,6 @@ def test_superblock_init_matches_oracle(dev):
 
 
 # ------------------------------------------------------------------ one step from a shared state
-def _warm(st, rng):
-    """A state with non-zero Adam moments (as after some steps)."""
-    st = st.copy()
-    st.m = (rng.standard_normal(st.m.shape) * 1e-3).astype(np.float32)
-    st.v = (rng.uniform(0.5, 2, st.v.shape) * 1e-6).astype(np.float32)
-    st.m_s = (rng.standard_normal(st.m_s.shape) * 1e-4).astype(np.float32)
-    st.v_s = (rng.uniform(0.5, 2, st.v_s.shape) * 1e-8).astype(np.float32)
-    st.t = 7
-    return st
-
-
 CASES = [
     # precision, batch, O, I, K, gs, layout, tau, kappa
     ("fp32", 1, 256, 256, 4, 128, "group", 0.05, 1.0),
@@ -297,25 +274,36 @@ def test_superblock_rejects_scale_training(dev):
 
 
 # ------------------------------------------------------------------ full size, sampled rows
-def test_full_size_attention_layer_on_sampled_rows(dev):
-    """The 4096 x 4096 ternary attention projection in the benchmark's launch configuration
-    (next sample drawn by the backward pass): init, two steps, sampled rows vs the oracle."""
-    w = inputs.WORKLOADS["attn-4096x4096-k3"]
+@pytest.mark.parametrize("name", ["attn-4096x4096-k3", "mlp-down-4096x14336-shift8",
+                                  "attn-4096x4096-ternary"])
+def test_full_size_layer_on_sampled_rows(dev, name):
+    """A full-size workload in the benchmark's launch configuration (next sample drawn by the
+    backward pass): init, two steps, sampled rows (first, last, interior) vs the oracle."""
+    w = inputs.WORKLOADS[name]
     W, Hd = inputs.make_layer(w, device=dev)
     H = Hd.cpu().numpy()
-    rcfg = ref.Config(w.out_features, w.in_features, w.levels, w.group_size, precision="bf16", seed=0)
+    alpha = 3.0 if w.relaxation == "ternary" else 6.0
+    rcfg = ref.Config(w.out_features, w.in_features, w.levels, w.group_size, precision="bf16",
+                      seed=0, layout=w.layout, relaxation=w.relaxation, alpha=alpha)
     pair_cfg = B.LayerConfig(w.out_features, w.in_features, w.levels, w.group_size,
-                             precision=B.PREC_BF16, seed=0)
+                             layout={"base3": B.LAYOUT_BASE3}.get(w.layout, B.LAYOUT_GROUP),
+                             precision=B.PREC_BF16, seed=0, alpha=alpha,
+                             relaxation={"shift": B.RELAX_SHIFT, "ternary": B.RELAX_TERNARY}.get(
+                                 w.relaxation, B.RELAX_GRID))
     layer = B.Layer(pair_cfg, torch.from_numpy(W).to(dev).to(torch.bfloat16), Hd)
-    rows = np.array([0, 1, 777, 2048, 4095])
+    O, I, K, gs = w.out_features, w.in_features, pair_cfg.K, w.group_size
+    rows = np.array([0, 1, 777, O // 2, O - 1])
     Hs = ref.symmetrize(H)
+    del H
     st = ref.init_layer(rcfg, W, rows=rows)
-    O, I, K = w.out_features, w.in_features, 3
     lg = torch.empty(1, O, I, K, device=dev)
-    sc = torch.empty(1, O, I // 128, device=dev)
-    layer.get_state(logits=lg, scales=sc)
+    sc = torch.empty(1, O, I // gs, device=dev)
+    base = torch.empty(1, O, I, dtype=torch.uint8, device=dev) if w.relaxation == "shift" else None
+    layer.get_state(logits=lg, scales=sc, base=base)
     np.testing.assert_array_equal(sc.cpu().numpy()[:, rows], st.scales)
     assert rel_err(lg.cpu().numpy()[:, rows], st.logits) <= 1e-6
+    if base is not None:
+        np.testing.assert_array_equal(base.cpu().numpy()[:, rows], st.base)
     T = w.steps
     for t in range(2):
         tau, nxt = ref.tau_schedule(t, T), ref.tau_schedule(t + 1, T)
@@ -327,12 +315,14 @@ def test_full_size_attention_layer_on_sampled_rows(dev):
         st_new, _, inter = ref.step(rcfg, W, Hs, st, oracle_params(prm), rows=rows, want=True)
         assert rel_err(G.cpu().numpy()[:, rows], inter["G"]) <= 1e-3
         got = {k: torch.empty(1, O, I, K, device=dev) for k in ("logits", "m", "v")}
-        got.update({k: torch.empty(1, O, I // 128, device=dev) for k in ("scales", "m_s", "v_s")})
+        got.update({k: torch.empty(1, O, I // gs, device=dev) for k in ("scales", "m_s", "v_s")})
         tt = layer.get_state(**got)
         gst = ref.State(*(got[k].cpu().numpy()[:, rows] for k in ("logits", "m", "v", "scales", "m_s", "v_s")), tt)
-        assert_state_close(gst, st_new, inter["G"], 1e-3, t + 1, label=f"full-size step {t}")
+        assert_state_close(gst, st_new, inter["G"], 1e-3, t + 1, label=f"{name} step {t}",
+                           dlogits=inter["dlogits"])
         assert np.isfinite(loss.item()) and loss.item() > 0
         st = st_new
+    layer.destroy()
 
 
 # ------------------------------------------------------------------ Lion (§3.3) and AdamW (App. B)
