@@ -96,7 +96,8 @@ void free_layer(gsq::Layer* L) {
   }
   for (hipEvent_t e : L->event_pool) (void)hipEventDestroy(e);
   void* bufs[] = {L->W, L->H, L->L, L->M, L->V, L->S, L->MS, L->VS, L->R[0], L->R[1],
-                  L->G, L->partials, L->flag, L->sb_d, L->sb_sc, L->codes, L->J0};
+                  L->G, L->partials, L->loss_part, L->loss_stage, L->loss_tickets, L->flag, L->sb_d, L->sb_sc, L->codes,
+                  L->J0};
   for (void* p : bufs)
     if (p) (void)hipFree(p);
   delete L;
@@ -213,12 +214,16 @@ gsq_status gsq_layer_init(const gsq_config* cfg, const void* W, int32_t w_dtype,
   const size_t relem = L.bf16 ? 2 : 4;
   const size_t npad = (size_t)(L.B * L.Opad * L.Ipad);
   L.tiles_per_batch = gsq::contract_tiles_per_batch(L);
+  L.loss_cols = (L.I + 255) / 256;
   bool ok = alloc(&L.W, L.N * (L.w_bf16 ? 2 : 4)) &&
             alloc(&L.H, (size_t)(L.B * L.Ipad * L.Ipad) * relem) &&
             alloc(&L.L, L.K * L.N * 4) && alloc(&L.M, L.K * L.N * 4) && alloc(&L.V, L.K * L.N * 4) &&
             alloc(&L.S, L.NG * 4) && alloc(&L.MS, L.NG * 4) && alloc(&L.VS, L.NG * 4) &&
             alloc(&L.R[0], npad * relem) && alloc(&L.R[1], npad * relem) &&
             alloc(&L.G, npad * 4) && alloc(&L.partials, (size_t)(L.B * L.tiles_per_batch) * 8) &&
+            alloc(&L.loss_part, (size_t)(L.B * L.O * L.loss_cols) * 8) &&
+            alloc(&L.loss_stage, (size_t)gsq::loss_stage_size(L) * 8) &&
+            alloc(&L.loss_tickets, (size_t)L.B * sizeof(unsigned)) &&
             alloc(&L.flag, sizeof(int)) && alloc(&L.codes, (size_t)L.N);
   if (ok && cfg->layout == GSQ_LAYOUT_SUPERBLOCK)
     ok = alloc(&L.sb_d, (L.N / 256) * 2) && alloc(&L.sb_sc, L.N / 16);
@@ -238,6 +243,7 @@ gsq_status gsq_layer_init(const gsq_config* cfg, const void* W, int32_t w_dtype,
     GSQ_HIP(hipMemsetAsync(L.MS, 0, L.NG * 4, stream));
     GSQ_HIP(hipMemsetAsync(L.VS, 0, L.NG * 4, stream));
     GSQ_HIP(hipMemsetAsync(L.flag, 0, sizeof(int), stream));
+    GSQ_HIP(hipMemsetAsync(L.loss_tickets, 0, (size_t)L.B * sizeof(unsigned), stream));
     float cmax = 0.f;
     for (int k = 0; k < L.n_grid; ++k) cmax = std::fmax(cmax, std::fabs(cfg->levels[k]));
     GSQ_HIP(timed(L, GSQ_KERNEL_INIT, stream, [&] { return gsq::launch_init_scales(L, scales_init, cmax, stream); }));
@@ -257,22 +263,15 @@ gsq_status gsq_layer_init(const gsq_config* cfg, const void* W, int32_t w_dtype,
   return GSQ_OK;
 }
 
-// Room for M per-sample gradients and loss partials (a step asking for more samples than
-// any before it); the old buffers are released after the device is idle.
+// Room for M per-sample gradients (a step asking for more samples than any before it); the
+// old buffer is released after the device is idle.
 static gsq_status grow_sample_slots(gsq::Layer& L, int M) {
   const size_t npad = (size_t)(L.B * L.Opad * L.Ipad);
   float* G = nullptr;
-  double* part = nullptr;
-  if (!alloc(&G, (size_t)M * npad * 4) ||
-      !alloc(&part, (size_t)M * L.B * L.tiles_per_batch * 8)) {
-    if (G) (void)hipFree(G);
-    return fail(GSQ_ENOMEM, "no room for %d samples", M);
-  }
-  GSQ_HIP(hipDeviceSynchronize());   // no launch on any stream still reads the old buffers
+  if (!alloc(&G, (size_t)M * npad * 4)) return fail(GSQ_ENOMEM, "no room for %d samples", M);
+  GSQ_HIP(hipDeviceSynchronize());   // no launch on any stream still reads the old buffer
   (void)hipFree(L.G);
-  (void)hipFree(L.partials);
   L.G = G;
-  L.partials = part;
   L.sample_slots = M;
   L.last = -1;
   return GSQ_OK;
@@ -331,9 +330,9 @@ gsq_status gsq_step(gsq_layer* h, const gsq_step_params* p, float* loss_out, hip
       a.sample = smp;
       GSQ_HIP(timed(L, GSQ_KERNEL_FORWARD, stream, [&] { return gsq::launch_forward(L, a, stream); }));
     }
-    GSQ_HIP(timed(L, GSQ_KERNEL_CONTRACT, stream, [&] { return gsq::launch_contract(L, L.R[use], loss_out != nullptr, smp, stream); }));
+    GSQ_HIP(timed(L, GSQ_KERNEL_CONTRACT, stream, [&] { return gsq::launch_contract(L, L.R[use], false, smp, stream); }));
   }
-  if (loss_out) GSQ_HIP(timed(L, GSQ_KERNEL_REDUCE, stream, [&] { return gsq::launch_reduce_loss(L, loss_out, M, stream); }));
+  a.want_loss = loss_out ? 1 : 0;   // the backward sums the loss terms of every sample
   a.sample = 0;
   a.samples = M;
   a.g_stride = L.B * L.Opad * L.Ipad;
@@ -359,6 +358,7 @@ gsq_status gsq_step(gsq_layer* h, const gsq_step_params* p, float* loss_out, hip
   a.inv_tau_n_d = a.fuse ? 1.0 / (double)p->tau_next : 0.0;
   a.Rout = L.R[1 - use];
   GSQ_HIP(timed(L, GSQ_KERNEL_BACKWARD, stream, [&] { return gsq::launch_backward(L, a, p->lr_scales > 0.f, stream); }));
+  if (loss_out) GSQ_HIP(timed(L, GSQ_KERNEL_REDUCE, stream, [&] { return gsq::launch_reduce_loss(L, loss_out, true, 1.0 / M, stream); }));
 
   L.last = use;
   L.last_sample = M - 1;
@@ -393,7 +393,7 @@ gsq_status gsq_harden(gsq_layer* h, uint8_t* codes, float* scales, float* hard_l
   GSQ_HIP(timed(L, GSQ_KERNEL_HARDEN, stream, [&] { return gsq::launch_eff_scales(L, scales, stream); }));
   if (hard_loss_out) {
     GSQ_HIP(timed(L, GSQ_KERNEL_CONTRACT, stream, [&] { return gsq::launch_contract(L, Rh, true, 0, stream); }));
-    GSQ_HIP(timed(L, GSQ_KERNEL_REDUCE, stream, [&] { return gsq::launch_reduce_loss(L, hard_loss_out, 1, stream); }));
+    GSQ_HIP(timed(L, GSQ_KERNEL_REDUCE, stream, [&] { return gsq::launch_reduce_loss(L, hard_loss_out, false, 1.0, stream); }));
     L.last = -1;   // G now belongs to the hard residual
     L.last_sample = 0;
   }

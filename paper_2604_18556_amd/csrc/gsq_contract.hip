@@ -8,6 +8,8 @@
 // FP32 precision: fp32 operands, fp64 accumulation on the vector units.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+
 #include "gsq_device.hpp"
 #include "gsq_internal.h"
 
@@ -53,7 +55,9 @@ __device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& 
 
 // One 256 x 256 tile of G per workgroup; four wavefronts each own 128 x 128 as 4 x 4 MFMA
 // 32x32x16 tiles.  K slabs 64 wide (whole 128-byte lines of R and H) stream through two LDS
-// buffers by direct global->LDS loads (16 bytes per lane, no staging registers).
+// buffers by direct global->LDS loads (16 bytes per lane, no staging registers).  The steady-
+// state loop has no branches, so the fragment reads and slab loads are spread between the
+// matrix-core instructions (scheduling groups) instead of stalling them.
 //
 // LDS layout of a slab: row r occupies 128 bytes as eight 16-byte chunks, chunk c stored at
 // position c ^ f(r), f(r) = (r ^ (r >> 3)) & 7.  The fragment reads (consecutive rows, one
@@ -61,16 +65,14 @@ __device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& 
 // banks.
 __device__ __forceinline__ int swz(int r) { return (r ^ (r >> 3)) & 7; }
 
-__device__ __forceinline__ void load_slab(const uint16_t* src, int64_t ld, int64_t k0,
-                                          uint8_t* lds, int wave, int lane) {
-  // wave w fills rows 64 w .. 64 w + 63, eight rows (1 KB of LDS) per instruction
+// Global->LDS copy of one operand's slab rows 64 w .. 64 w + 63 (wave w): eight instructions of
+// eight rows, 16 bytes per lane.  `src` is wave-uniform (the slab's first column); off[j] is the
+// lane's element offset of instruction j, fixed for the whole K loop.
+__device__ __forceinline__ void load_slab(const uint16_t* src, const uint32_t (&off)[8],
+                                          uint8_t* lds_wave) {
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int row = wave * 64 + j * 8 + (lane >> 3);
-    const int chunk = (lane & 7) ^ swz(row);
-    const uint16_t* g = src + row * ld + k0 + chunk * 8;
-    __builtin_amdgcn_global_load_lds(g, lds + (wave * 64 + j * 8) * ROW_BYTES, 16, 0, 0);
-  }
+  for (int j = 0; j < 8; ++j)
+    __builtin_amdgcn_global_load_lds(src + off[j], lds_wave + j * 8 * ROW_BYTES, 16, 0, 0);
 }
 
 __device__ __forceinline__ bf16x8 read_frag(const uint8_t* lds, int row, int chunk) {
@@ -84,13 +86,19 @@ __device__ __forceinline__ void wait_vm() {
   __builtin_amdgcn_s_waitcnt((n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14));
 }
 
-// Workgroup barrier for the slab ring.  The wavefront's own global->LDS loads have been
-// waited for (wait_vm) and its LDS reads are drained here; a plain s_barrier then suffices.
-// (__syncthreads would also drain every in-flight slab of the ring.)  The memory clobber
-// keeps the compiler from moving LDS accesses across it.
+// Workgroup barrier for the slab ring: this wavefront's LDS reads are drained (its own
+// global->LDS loads were waited for with wait_vm), then a plain s_barrier.  The signal fences
+// keep the compiler from moving memory accesses across it; the waits are real instructions, so
+// the compiler's own wait bookkeeping sees them.
 __device__ __forceinline__ void slab_barrier() {
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt((15) | (7 << 4) | (0 << 8) | (3 << 14));   // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
+
+// scheduling-group masks
+constexpr int SG_MFMA = 0x008, SG_VMEM = 0x020, SG_DSR = 0x100;
 
 __global__ __launch_bounds__(256, 1) void k_contract_bf16(const uint16_t* __restrict__ R,
                                                           const uint16_t* __restrict__ H,
@@ -105,7 +113,8 @@ __global__ __launch_bounds__(256, 1) void k_contract_bf16(const uint16_t* __rest
   const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
   const uint16_t* A = R + b * Opad * Ipad + m0 * Ipad;
   const uint16_t* Bt = H + b * Ipad * Ipad + n0 * Ipad;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
 
   f32x16 acc[4][4];
@@ -116,12 +125,21 @@ __global__ __launch_bounds__(256, 1) void k_contract_bf16(const uint16_t* __rest
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  const int64_t nk = Ipad / BK;   // a multiple of 4 (Ipad is a multiple of 256)
-  auto issue = [&](int64_t k) {
-    uint8_t* st = smem + (k % STAGES) * 2 * SLAB_BYTES;
-    load_slab(A, Ipad, k * BK, st, wave, lane);
-    load_slab(Bt, Ipad, k * BK, st + SLAB_BYTES, wave, lane);
-  };
+  // lane offsets of the slab copies: row 64 wave + 8 j + lane / 8, swizzled 16-byte chunk
+  uint32_t off[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int row = wave * 64 + j * 8 + (lane >> 3);
+    // < 256 Ipad + 64 <= 2^32 for the widest layer the library accepts (I <= 2^24)
+    off[j] = (uint32_t)row * (uint32_t)Ipad + (uint32_t)(((lane & 7) ^ swz(row)) * 8);
+  }
+  const int nk = (int)(Ipad / BK);   // a multiple of 4 (Ipad is a multiple of 256)
+#define GSQ_ISSUE(K)                                                                     \
+  do {                                                                                   \
+    uint8_t* st_ = smem + ((K) % STAGES) * 2 * SLAB_BYTES + wave * 64 * ROW_BYTES;       \
+    load_slab(A + (int64_t)(K) * BK, off, st_);                                          \
+    load_slab(Bt + (int64_t)(K) * BK, off, st_ + SLAB_BYTES);                            \
+  } while (0)
   const int frow_a = wm * 128 + (lane & 31), frow_b = wn * 128 + (lane & 31);
   const int fchunk = lane >> 5;
 
@@ -142,30 +160,63 @@ __global__ __launch_bounds__(256, 1) void k_contract_bf16(const uint16_t* __rest
     _Pragma("unroll") for (int i = 0; i < 4; ++i)                                        \
       _Pragma("unroll") for (int j = 0; j < 4; ++j)                                      \
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(S##a[h][i], S##b[h][j], acc[i][j], 0, 0, 0)
+// interleave: 16 x (one MFMA, one LDS read), then 16 MFMAs
+#define GSQ_SCHED_READS()                                                                \
+  _Pragma("unroll") for (int i_ = 0; i_ < 16; ++i_) {                                    \
+    __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);                                 \
+    __builtin_amdgcn_sched_group_barrier(SG_DSR, 1, 0);                                  \
+  }                                                                                      \
+  __builtin_amdgcn_sched_group_barrier(SG_MFMA, 16, 0)
+// interleave: 16 x (one MFMA, one LDS read), then 16 x (one MFMA, one global->LDS load): the
+// next slab's fragments arrive early, the loads have a whole slab of time to land
+#define GSQ_SCHED_LOADS_READS()                                                          \
+  _Pragma("unroll") for (int i_ = 0; i_ < 16; ++i_) {                                    \
+    __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);                                 \
+    __builtin_amdgcn_sched_group_barrier(SG_DSR, 1, 0);                                  \
+  }                                                                                      \
+  _Pragma("unroll") for (int i_ = 0; i_ < 16; ++i_) {                                    \
+    __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);                                 \
+    __builtin_amdgcn_sched_group_barrier(SG_VMEM, 1, 0);                                 \
+  }
 
   // p: first half (sub-steps 0, 1) of the current slab; q: second half (sub-steps 2, 3)
   bf16x8 pa[2][4], pb[2][4], qa[2][4], qb[2][4];
-  issue(0);
-  issue(1);
+  GSQ_ISSUE(0);
+  GSQ_ISSUE(1);
   wait_vm<LOADS_PER_STAGE>();
   slab_barrier();
   GSQ_READ(p, 0, 0);
-  for (int64_t kt = 0; kt < nk; ++kt) {
-    // phase 1: read the second half of slab kt while its first half feeds the matrix cores
+  // steady state: no branches, so loads and reads interleave with the matrix-core work
+  for (int kt = 0; kt < nk - 2; ++kt) {
     GSQ_READ(q, kt, 1);
     GSQ_MFMA(p);
-    // phase 2: slab kt+1 (issued one slab ago) must have landed, and every wavefront's reads
-    // of slab kt must have returned before its buffer is refilled with slab kt+2
-    if (kt + 1 < nk) {
-      wait_vm<0>();
-      slab_barrier();
-      if (kt + 2 < nk) issue(kt + 2);
-      GSQ_READ(p, kt + 1, 0);
-    }
+    GSQ_SCHED_READS();
+    __builtin_amdgcn_sched_barrier(0);   // every MFMA of this half is issued before the wait
+    // slab kt+1 (issued one slab ago) has landed, and every wavefront has read slab kt, whose
+    // buffer is then refilled with slab kt+2
+    wait_vm<0>();
+    slab_barrier();
+    GSQ_READ(p, kt + 1, 0);
+    GSQ_ISSUE(kt + 2);
     GSQ_MFMA(q);
+    GSQ_SCHED_LOADS_READS();
+    __builtin_amdgcn_sched_barrier(0);
   }
+  // the last two slabs: nothing more to load
+  GSQ_READ(q, nk - 2, 1);
+  GSQ_MFMA(p);
+  wait_vm<0>();
+  slab_barrier();
+  GSQ_READ(p, nk - 1, 0);
+  GSQ_MFMA(q);
+  GSQ_READ(q, nk - 1, 1);
+  GSQ_MFMA(p);
+  GSQ_MFMA(q);
+#undef GSQ_SCHED_LOADS_READS
+#undef GSQ_SCHED_READS
 #undef GSQ_MFMA
 #undef GSQ_READ
+#undef GSQ_ISSUE
 
   // 32 x 32 accumulator layout: lane l, register r -> row 8*(r/4) + 4*(l/32) + r%4, column l%32
   float* Gb = G + b * Opad * Ipad;
@@ -241,25 +292,57 @@ __global__ __launch_bounds__(256) void k_contract_f32(const float* __restrict__ 
     block_sum_to(lsum, partials + (b * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x);
 }
 
-// Loss of layer b = mean over the samples of the sum of its tile partials, in a fixed order.
-// Partials of sample m, layer b start at (m * B + b) * per_batch.
-__global__ void k_reduce_loss(const double* partials, int64_t per_batch, int64_t B, int samples,
-                              float* loss_out, int* flag) {
-  const int64_t b = blockIdx.x;
-  double s = 0.0;
-  for (int m = 0; m < samples; ++m)
-    for (int64_t i = threadIdx.x; i < per_batch; i += 256) s += partials[(m * B + b) * per_batch + i];
+// Loss of layer b = scale * the sum of its per_batch partials, in a fixed order, in one launch:
+// block (c, b) sums chunk c (kChunk consecutive partials) into stage[b * nchunks + c]; the last
+// block of layer b to finish (a ticket counter, reset by that block) sums the chunks in order.
+constexpr int kPer = 8;                 // partials per thread, all loaded before summing
+constexpr int kChunk = 256 * kPer;
+
+__device__ __forceinline__ double block_tree_sum(double x) {
   __shared__ double red[256];
-  red[threadIdx.x] = s;
+  red[threadIdx.x] = x;
   __syncthreads();
   for (int w = 128; w > 0; w >>= 1) {
     if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
     __syncthreads();
   }
+  const double r = red[0];
+  __syncthreads();
+  return r;
+}
+
+__global__ void k_reduce_loss(const double* partials, int64_t per_batch, int nchunks,
+                              double* stage, unsigned* tickets, double scale, float* loss_out,
+                              int* flag) {
+  const int64_t b = blockIdx.y, c = blockIdx.x;
+  const int64_t lo = c * kChunk, hi = min(per_batch, lo + kChunk);
+  double v[kPer];
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int64_t i = lo + threadIdx.x + 256 * j;
+    v[j] = i < hi ? partials[b * per_batch + i] : 0.0;
+  }
+  double s = 0.0;
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) s += v[j];
+  const double tot = block_tree_sum(s);
+  __shared__ unsigned ticket;
   if (threadIdx.x == 0) {
-    const float L = (float)(red[0] / samples);
+    stage[b * nchunks + c] = tot;
+    __threadfence();                       // the chunk sum is visible before the ticket
+    ticket = atomicAdd(&tickets[b], 1u);
+  }
+  __syncthreads();
+  if (ticket != (unsigned)(nchunks - 1)) return;
+  __threadfence();
+  double t = 0.0;
+  for (int i = threadIdx.x; i < nchunks; i += 256) t += __builtin_nontemporal_load(&stage[b * nchunks + i]);
+  const double all = block_tree_sum(t);
+  if (threadIdx.x == 0) {
+    const float L = (float)(all * scale);
     loss_out[b] = L;
     if (!__builtin_isfinite(L)) *flag = 1;
+    tickets[b] = 0u;
   }
 }
 
@@ -271,7 +354,7 @@ int64_t contract_tiles_per_batch(const Layer& L) {
 
 hipError_t launch_contract(const Layer& L, const void* R, bool want_loss, int slot, hipStream_t s) {
   float* G = L.G + (int64_t)slot * L.B * L.Opad * L.Ipad;
-  double* partials = L.partials + (int64_t)slot * L.B * L.tiles_per_batch;
+  double* partials = L.partials;
   if (L.bf16) {
     static bool attr_set = false;
     if (!attr_set) {
@@ -294,9 +377,18 @@ hipError_t launch_contract(const Layer& L, const void* R, bool want_loss, int sl
   return hipGetLastError();
 }
 
-hipError_t launch_reduce_loss(const Layer& L, float* loss_out, int samples, hipStream_t s) {
-  hipLaunchKernelGGL(k_reduce_loss, dim3((unsigned)L.B), dim3(256), 0, s, L.partials,
-                     contract_tiles_per_batch(L), L.B, samples, loss_out, L.flag);
+int64_t loss_stage_size(const Layer& L) {
+  const int64_t most = std::max<int64_t>(L.O * L.loss_cols, contract_tiles_per_batch(L));
+  return L.B * ((most + kChunk - 1) / kChunk);
+}
+
+hipError_t launch_reduce_loss(const Layer& L, float* loss_out, bool from_rows, double scale,
+                              hipStream_t s) {
+  const double* part = from_rows ? L.loss_part : L.partials;
+  const int64_t per_batch = from_rows ? L.O * L.loss_cols : contract_tiles_per_batch(L);
+  const int nchunks = (int)((per_batch + kChunk - 1) / kChunk);
+  hipLaunchKernelGGL(k_reduce_loss, dim3((unsigned)nchunks, (unsigned)L.B), dim3(256), 0, s, part,
+                     per_batch, nchunks, L.loss_stage, L.loss_tickets, scale, loss_out, L.flag);
   return hipGetLastError();
 }
 

@@ -62,6 +62,13 @@ __device__ __forceinline__ void store_r4(void* R, int64_t idx, const float (&r)[
   }
 }
 
+// R = W - s v before the contraction's rounding; the forward, the fused next sample and the
+// backward's loss all form it with this one expression.
+template <bool kF64>
+__device__ __forceinline__ float residual(float w, Real<kF64> s, Real<kF64> v) {
+  return (float)((Real<kF64>)w - s * v);
+}
+
 // fp32 path: hardware exp2 / reciprocal / square root (about 1 ulp); fp64 path: libm.
 constexpr float kLog2e = 1.4426950408889634f;
 __device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
@@ -175,26 +182,29 @@ __device__ __forceinline__ void fill_windows(float* win, const ElemArgs& a) {
   __syncthreads();
 }
 
-// The values the logits of the chunk's four coordinates stand for.
+// Base indices of the chunk's four coordinates (local shift; one byte each), or 0.
+template <int kMode>
+__device__ __forceinline__ uint32_t chunk_bases(const ElemArgs& a, int64_t e0) {
+  if constexpr (kMode == GSQ_RELAX_SHIFT) return *reinterpret_cast<const uint32_t*>(a.J0 + e0);
+  else return 0u;
+}
+
+// The values the logits of coordinate q of the chunk stand for: the grid (GRID), or the
+// window of its base index read from the LDS table (SHIFT; read where needed rather than
+// held in registers).
 template <int K, int kMode>
-__device__ __forceinline__ void chunk_candidates(float (&cand)[4][K], const ElemArgs& a, const float* win,
-                                                 int64_t e0) {
+__device__ __forceinline__ void coord_candidates(float (&cand)[K], const ElemArgs& a, const float* win,
+                                                 uint32_t j4, int q) {
   if constexpr (kMode == GSQ_RELAX_SHIFT) {
     static_assert(K == GSQ_SHIFT_WINDOW, "five shifts");
-    const uint32_t j4 = *reinterpret_cast<const uint32_t*>(a.J0 + e0);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      int j = (int)((j4 >> (8 * q)) & 0xFFu);
-      j = j < a.n_grid ? j : a.n_grid - 1;          // a corrupt index cannot leave the table
-      const float4 lo = *reinterpret_cast<const float4*>(win + j * kWinRow);
-      cand[q][0] = lo.x; cand[q][1] = lo.y; cand[q][2] = lo.z; cand[q][3] = lo.w;
-      cand[q][4] = win[j * kWinRow + 4];
-    }
+    int j = (int)((j4 >> (8 * q)) & 0xFFu);
+    j = j < a.n_grid ? j : a.n_grid - 1;          // a corrupt index cannot leave the table
+    const float4 lo = *reinterpret_cast<const float4*>(win + j * kWinRow);
+    cand[0] = lo.x; cand[1] = lo.y; cand[2] = lo.z; cand[3] = lo.w;
+    cand[4] = win[j * kWinRow + 4];
   } else {
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-#pragma unroll
-      for (int k = 0; k < K; ++k) cand[q][k] = a.c[k];
+    for (int k = 0; k < K; ++k) cand[k] = a.c[k];
   }
 }
 
@@ -233,19 +243,19 @@ __global__ __launch_bounds__(kBlock) void k_forward(ElemArgs a) {
     float4 lv[K];
 #pragma unroll
     for (int k = 0; k < K; ++k) lv[k] = *reinterpret_cast<const float4*>(a.L + k * a.N + e0);
-    float cand[4][K];
-    chunk_candidates<K, kMode>(cand, a, win, e0);
+    const uint32_t j4 = chunk_bases<kMode>(a, e0);
     float g[4][Z];
     chunk_noise<Z, kF64>(g, a, (uint64_t)e0, a.t, (uint32_t)a.sample);
     float r[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      float l[K];
+      float l[K], cand[K];
 #pragma unroll
       for (int k = 0; k < K; ++k) l[k] = f4get(lv[k], q);
+      coord_candidates<K, kMode>(cand, a, win, j4, q);
       T v, jac[K];
-      coord_sample<K, Z, kF64, kMode>(l, cand[q], g[q], a.kappa, inv_tau, v, jac);
-      r[q] = (float)((T)w[q] - s * v);
+      coord_sample<K, Z, kF64, kMode>(l, cand, g[q], a.kappa, inv_tau, v, jac);
+      r[q] = residual<kF64>(w[q], s, v);
     }
     store_r4<kF64>(a.Rout, padded_index(a, row, col0), r);
   }
@@ -274,10 +284,44 @@ __device__ __forceinline__ void opt_update(bool lion, Real<kF64> d, Real<kF64>& 
   }
 }
 
+// x shifted up by n lanes within each 16-lane row (lanes below the row start read 0).
+template <int kCtrl>
+__device__ __forceinline__ double dpp_shr(double x) {
+  const uint64_t b = __double_as_longlong(x);
+  const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, kCtrl, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(b >> 32), kCtrl, 0xF, 0xF, false);
+  return __longlong_as_double((long long)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo));
+}
+
+// x from lane 15 of the previous 16-lane row (kCtrl = row broadcast 15) or from lane 31
+// (row broadcast 31), added only in the rows of kRows; other lanes read 0.
+template <int kCtrl, int kRows>
+__device__ __forceinline__ double dpp_bcast(double x) {
+  const uint64_t b = __double_as_longlong(x);
+  const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, kCtrl, kRows, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(b >> 32), kCtrl, kRows, 0xF, false);
+  return __longlong_as_double((long long)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo));
+}
+
+// Sum over the wavefront in a fixed order, left in lane 63: prefix sums within each 16-lane
+// row (shifts by 1, 2, 4, 8), then row 0's total into row 1 and row 2's into row 3, then the
+// first half's total into the second half.
+__device__ __forceinline__ double wave_sum_to_lane63(double x) {
+  x += dpp_shr<0x111>(x);
+  x += dpp_shr<0x112>(x);
+  x += dpp_shr<0x114>(x);
+  x += dpp_shr<0x118>(x);
+  x += dpp_bcast<0x142, 0xA>(x);
+  x += dpp_bcast<0x143, 0xC>(x);
+  return x;
+}
+
 // ------------------------------------------------------------------ gradient + update (+ next sample)
 // dL/dl_k = (kappa / tau) G s p_k (c_k - v); dL/ds = sum over the group of G v.  Adam (bias
 // correction at step n = t + 1) or Lion.  With a.fuse, the sample of step t + 1 is drawn from
-// the updated logits and scale and its residual written to a.Rout.
+// the updated logits and scale and its residual written to a.Rout.  With a.want_loss, the
+// loss terms R * P = R * (-G / 2) of this step's sample(s) are summed per row and 256-column
+// block (R rebuilt exactly as the contraction saw it) into a.loss_part.
 template <int K, bool kF64, bool kScales, bool kMulti, int kMode>
 __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
   using T = Real<kF64>;
@@ -306,20 +350,14 @@ __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
     const T s = (T)s32;
     float4 lv[K], mv[K], vv[K];
     const int64_t gidx = active ? padded_index(a, row, col0) : 0;
-    if (active) {
 #pragma unroll
-      for (int k = 0; k < K; ++k) {
-        lv[k] = *reinterpret_cast<const float4*>(a.L + k * a.N + e0);
-        mv[k] = *reinterpret_cast<const float4*>(a.M + k * a.N + e0);
-        vv[k] = lion ? make_float4(0.f, 0.f, 0.f, 0.f)
-                     : *reinterpret_cast<const float4*>(a.V + k * a.N + e0);
-      }
-    } else {
-#pragma unroll
-      for (int k = 0; k < K; ++k) lv[k] = mv[k] = vv[k] = make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-    float cand[4][K];
-    chunk_candidates<K, kMode>(cand, a, win, e0);
+    for (int k = 0; k < K; ++k)
+      lv[k] = active ? *reinterpret_cast<const float4*>(a.L + k * a.N + e0)
+                     : make_float4(0.f, 0.f, 0.f, 0.f);
+    const uint32_t j4 = chunk_bases<kMode>(a, e0);
+    float w[4] = {0.f, 0.f, 0.f, 0.f};
+    if (active && (a.want_loss || a.fuse)) load_w4(a.W, a.w_bf16, e0, w);
+    T lacc = 0;   // sum of R G over the thread's coordinates and samples
     // gradient, averaged over the step's independent samples (one unless kMulti)
     T ds_part = 0;
     T dacc[4][K];
@@ -335,17 +373,28 @@ __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
       chunk_noise<Z, kF64>(g, a, (uint64_t)e0, a.t, (uint32_t)smp);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        float l[K];
+        float l[K], cand[K];
 #pragma unroll
         for (int k = 0; k < K; ++k) l[k] = f4get(lv[k], q);
+        coord_candidates<K, kMode>(cand, a, win, j4, q);
         T v, jac[K];
-        coord_sample<K, Z, kF64, kMode>(l, cand[q], g[q], a.kappa, inv_tau, v, jac);
+        coord_sample<K, Z, kF64, kMode>(l, cand, g[q], a.kappa, inv_tau, v, jac);
         const T gq = (T)f4get(gv, q);
         ds_part += gq * v;
         const T coef = kt * (gq * s);
 #pragma unroll
         for (int k = 0; k < K; ++k) dacc[q][k] += coef * jac[k];
+        if (a.want_loss) {
+          float r = residual<kF64>(w[q], s, v);
+          if constexpr (!kF64) r = bf16_to_f32(bf16_rne(r));
+          lacc += (T)r * gq;
+        }
       }
+    }
+    if (a.want_loss) {
+      // P = -G / 2; the wavefront's sum (one row, 256 columns) in a fixed order
+      const double lsum = wave_sum_to_lane63(-0.5 * (double)lacc);
+      if (lane == 63) a.loss_part[row * gridDim.x + blockIdx.x] = lsum;
     }
     if constexpr (kMulti) {
       const T inv_m = T(1) / (T)M;
@@ -354,6 +403,15 @@ __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
       for (int q = 0; q < 4; ++q)
 #pragma unroll
         for (int k = 0; k < K; ++k) dacc[q][k] *= inv_m;
+    }
+    // the moments are needed only by the update: loading them here keeps them out of the
+    // registers of the sample loop
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      mv[k] = active ? *reinterpret_cast<const float4*>(a.M + k * a.N + e0)
+                     : make_float4(0.f, 0.f, 0.f, 0.f);
+      vv[k] = (active && !lion) ? *reinterpret_cast<const float4*>(a.V + k * a.N + e0)
+                                : make_float4(0.f, 0.f, 0.f, 0.f);
     }
 #pragma unroll
     for (int q = 0; q < 4; ++q)
@@ -397,19 +455,18 @@ __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
     }
     if (a.fuse && active) {
       const T inv_tau_n = kF64 ? (T)a.inv_tau_n_d : (T)a.inv_tau_n;
-      float w[4];
-      load_w4(a.W, a.w_bf16, e0, w);
       float g[4][Z];
       chunk_noise<Z, kF64>(g, a, (uint64_t)e0, a.t_next, 0u);
       float r[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        float l[K];
+        float l[K], cand[K];
 #pragma unroll
         for (int k = 0; k < K; ++k) l[k] = f4get(lv[k], q);
+        coord_candidates<K, kMode>(cand, a, win, j4, q);
         T v, jac[K];
-        coord_sample<K, Z, kF64, kMode>(l, cand[q], g[q], a.kappa_n, inv_tau_n, v, jac);
-        r[q] = (float)((T)w[q] - (T)s_new * v);
+        coord_sample<K, Z, kF64, kMode>(l, cand, g[q], a.kappa_n, inv_tau_n, v, jac);
+        r[q] = residual<kF64>(w[q], (T)s_new, v);
       }
       store_r4<kF64>(a.Rout, padded_index(a, row, col0), r);
     }
@@ -721,6 +778,7 @@ ElemArgs base_args(const Layer& L) {
   a.L = L.L; a.M = L.M; a.V = L.V;
   a.S = L.S; a.MS = L.MS; a.VS = L.VS;
   a.flag = L.flag;
+  a.loss_part = L.loss_part;
   a.N = L.N;
   a.rows = (int32_t)(L.B * L.O);
   a.O = (int32_t)L.O; a.I = (int32_t)L.I;

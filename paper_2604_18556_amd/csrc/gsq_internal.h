@@ -23,6 +23,8 @@ struct ElemArgs {
   const uint8_t* J0;    // local shift: initial grid index of every coordinate (N bytes)
   float *S, *MS, *VS;   // one per scale group
   int* flag;            // sticky non-finite flag
+  double* loss_part;    // backward: loss partial of (row, 256-column block), when want_loss
+  int32_t want_loss;
   int64_t N;            // B*O*I
   int32_t rows;         // B*O
   int32_t O, I, Opad, Ipad, gs, w_bf16;
@@ -61,8 +63,12 @@ struct Layer {
   float *S = nullptr, *MS = nullptr, *VS = nullptr;
   void* R[2] = {nullptr, nullptr};
   float* G = nullptr;          // one padded gradient per sample slot
-  double* partials = nullptr;  // loss partials, per sample slot
-  int sample_slots = 1;        // capacity of G and partials in samples
+  double* partials = nullptr;  // loss partials of the contraction tiles (hard loss)
+  double* loss_part = nullptr; // loss partials of the backward, one per row and 256 columns
+  int64_t loss_cols = 0;       // 256-column blocks per row
+  double* loss_stage = nullptr;    // chunk sums of the loss reduction
+  unsigned* loss_tickets = nullptr;  // per layer: chunks summed so far (zero between launches)
+  int sample_slots = 1;        // capacity of G in samples
   int last_sample = 0;         // slot holding the most recent step's last sample
   int64_t tiles_per_batch = 0;
   int* flag = nullptr;
@@ -104,7 +110,11 @@ ElemArgs base_args(const Layer& L);
 
 // ---- launchers (gsq_contract.hip)
 int64_t contract_tiles_per_batch(const Layer& L);
+int64_t loss_stage_size(const Layer& L);   // doubles
 hipError_t launch_contract(const Layer& L, const void* R, bool want_loss, int slot, hipStream_t s);
-hipError_t launch_reduce_loss(const Layer& L, float* loss_out, int samples, hipStream_t s);
+// Loss of each layer from the contraction's tile partials (slot 0) or, with from_rows, from the
+// backward's row partials, times `scale`.
+hipError_t launch_reduce_loss(const Layer& L, float* loss_out, bool from_rows, double scale,
+                              hipStream_t s);
 
 }  // namespace gsq
