@@ -284,18 +284,21 @@ def coord_index(cfg, b, rows):
     return ((b * cfg.out_features + rows)[:, None] * cfg.in_features + i[None, :]).reshape(-1)
 
 
-def init_layer(cfg, W, scales_init=None, rows=None):
+def init_layer(cfg, W, scales_init=None, rows=None, batches=None):
     """Initial state of ``gsq_layer_init``: scales, RTN codes, logits, zero moments.
 
-    ``rows`` restricts the state to a subset of the rows of every layer (every
-    quantity of the initialisation is row-local); noise indices stay global.
+    ``rows`` restricts the state to a subset of the rows of every layer and
+    ``batches`` to a subset of the layers (every quantity of the initialisation is
+    row-local); noise indices stay global.
     """
     W = np.asarray(W, dtype=np.float64).reshape(cfg.batch, cfg.out_features, cfg.in_features)
     B, O, I, K = cfg.batch, cfg.out_features, cfg.in_features, cfg.K
     rows = np.arange(O) if rows is None else np.asarray(rows)
-    W = W[:, rows]
+    batches = np.arange(B) if batches is None else np.asarray(batches)
+    W = W[batches][:, rows]
     if scales_init is not None:
-        scales_init = np.asarray(scales_init, np.float32).reshape(B, O, I // cfg.gs)[:, rows]
+        scales_init = np.asarray(scales_init, np.float32).reshape(B, O, I // cfg.gs)[batches][:, rows]
+    B = len(batches)
     O = len(rows)
     sb_d = sb_sc = None
     if cfg.layout == "superblock":
@@ -308,12 +311,12 @@ def init_layer(cfg, W, scales_init=None, rows=None):
     if cfg.n_grid > 255:
         raise ValueError("grid too large")
     logits = np.empty((B, O, I, K), dtype=np.float32)
-    for b in range(B):
+    for j, b in enumerate(batches):
         eps = None
         if cfg.init_noise:
             e = coord_index(cfg, b, rows)
             eps = philox.init_normals(cfg.seed, e, K).reshape(O, I, K)
-        logits[b] = init_logits(q0[b], cfg, eps)
+        logits[j] = init_logits(q0[j], cfg, eps)
     z = np.zeros_like(logits)
     zs = np.zeros_like(scales)
     st = State(logits, z, z.copy(), scales.astype(np.float32), zs, zs.copy(), 0, sb_d, sb_sc)
@@ -485,7 +488,7 @@ def update(prm, theta, m, v, grad, lr, n):
     return adam(theta, m, v, grad, lr, prm.beta1, prm.beta2, prm.eps, n, prm.weight_decay)
 
 
-def step(cfg, W, Hs, st, prm, rows=None, want=False):
+def step(cfg, W, Hs, st, prm, rows=None, want=False, batches=None):
     """One GSQ optimisation step on state ``st`` (returns a new state, the loss).
 
     Order: noise -> soft sample -> residual -> contraction and loss -> gradient
@@ -496,7 +499,8 @@ def step(cfg, W, Hs, st, prm, rows=None, want=False):
     taken before the update, averaged over the step's samples.
 
     ``rows`` restricts the step to a subset of the rows of every layer (rows
-    are independent given H); ``st`` then holds just those rows and noise
+    are independent given H) and ``batches`` to a subset of the layers; ``st``
+    then holds just those rows and layers, ``Hs`` just those layers' H, and noise
     indices stay the global ones.
     ``want`` returns the intermediates (g, p, v, R, G of the last sample; the averaged
     dlogits, dscales).
@@ -504,14 +508,15 @@ def step(cfg, W, Hs, st, prm, rows=None, want=False):
     B, O, I, K = cfg.batch, cfg.out_features, cfg.in_features, cfg.K
     prm = as_f32_params(prm)
     rows = np.arange(O) if rows is None else np.asarray(rows)
-    W = np.asarray(W, np.float64).reshape(B, O, I)[:, rows]
-    Hs = np.asarray(Hs).reshape(B, I, I)
+    batches = np.arange(B) if batches is None else np.asarray(batches)
+    W = np.asarray(W, np.float64).reshape(B, O, I)[batches][:, rows]
+    Hs = np.asarray(Hs).reshape(len(batches), I, I)
     n = st.t + 1
     new = st.copy()
-    losses = np.zeros(B)
+    losses = np.zeros(len(batches))
     inter = {k: [] for k in ("g", "p", "v", "R", "G", "dlogits", "dscales")}
-    for b in range(B):
-        e = coord_index(cfg, b, rows)
+    for b, bg in enumerate(batches):
+        e = coord_index(cfg, bg, rows)
         lg = st.logits[b]
         sc = st.scales[b]
         s_coord = expand_scales(sc, cfg.gs)

@@ -102,6 +102,8 @@ CASES = [
     ("bf16", 1, 130, 512, 8, 128, "group", 0.2, 1.0),
     ("bf16", 1, 96, 256, 4, 64, "group", 0.5, 3.0),
     ("bf16", 3, 40, 512, 8, 16, "superblock", 0.3, 1.0),
+    ("fp32", 1, 1, 16, 3, 16, "group", 0.5, 1.0),       # one row, 16 columns: almost all padding
+    ("bf16", 5, 7, 48, 4, 16, "group", 0.3, 1.0),       # five small layers, ragged everywhere
 ]
 
 
@@ -274,53 +276,77 @@ def test_superblock_rejects_scale_training(dev):
 
 
 # ------------------------------------------------------------------ full size, sampled rows
-@pytest.mark.parametrize("name", ["attn-4096x4096-k3", "mlp-down-4096x14336-shift8",
-                                  "attn-4096x4096-ternary"])
+FULL_SIZE = ["attn-4096x4096-k3", "attn-4096x4096-ternary", "mlp-up-14336x4096-k8",
+             "mlp-down-4096x14336-k8", "mlp-down-4096x14336-shift8", "down-8192x28672-k4",
+             "moe-64x2048x7168-superblock"]
+
+
+@pytest.mark.parametrize("name", FULL_SIZE)
 def test_full_size_layer_on_sampled_rows(dev, name):
     """A full-size workload in the benchmark's launch configuration (next sample drawn by the
-    backward pass): init, two steps, sampled rows (first, last, interior) vs the oracle."""
+    backward pass, loss every step): init and two steps, sampled rows (first, second, interior,
+    middle, last) of sampled experts vs the oracle."""
     w = inputs.WORKLOADS[name]
     W, Hd = inputs.make_layer(w, device=dev)
-    H = Hd.cpu().numpy()
+    experts = [0] if w.batch == 1 else [0, 37, w.batch - 1]
+    Hs = ref.symmetrize(Hd[experts].cpu().numpy())
     alpha = 3.0 if w.relaxation == "ternary" else 6.0
-    rcfg = ref.Config(w.out_features, w.in_features, w.levels, w.group_size, precision="bf16",
-                      seed=0, layout=w.layout, relaxation=w.relaxation, alpha=alpha)
-    pair_cfg = B.LayerConfig(w.out_features, w.in_features, w.levels, w.group_size,
-                             layout={"base3": B.LAYOUT_BASE3}.get(w.layout, B.LAYOUT_GROUP),
-                             precision=B.PREC_BF16, seed=0, alpha=alpha,
+    rcfg = ref.Config(w.out_features, w.in_features, w.levels, w.group_size, batch=w.batch,
+                      precision="bf16", seed=0, layout=w.layout, relaxation=w.relaxation,
+                      alpha=alpha)
+    layouts = {"base3": B.LAYOUT_BASE3, "superblock": B.LAYOUT_SUPERBLOCK}
+    pair_cfg = B.LayerConfig(w.out_features, w.in_features, w.levels, w.group_size, w.batch,
+                             layouts.get(w.layout, B.LAYOUT_GROUP), B.PREC_BF16, seed=0,
+                             alpha=alpha,
                              relaxation={"shift": B.RELAX_SHIFT, "ternary": B.RELAX_TERNARY}.get(
                                  w.relaxation, B.RELAX_GRID))
     layer = B.Layer(pair_cfg, torch.from_numpy(W).to(dev).to(torch.bfloat16), Hd)
-    O, I, K, gs = w.out_features, w.in_features, pair_cfg.K, w.group_size
+    torch.cuda.synchronize()
+    del Hd                                   # the library keeps its own copy of H
+    torch.cuda.empty_cache()
+    Bn, O, I, K, gs = w.batch, w.out_features, w.in_features, pair_cfg.K, pair_cfg.gs
     rows = np.array([0, 1, 777, O // 2, O - 1])
-    Hs = ref.symmetrize(H)
-    del H
-    st = ref.init_layer(rcfg, W, rows=rows)
-    lg = torch.empty(1, O, I, K, device=dev)
-    sc = torch.empty(1, O, I // gs, device=dev)
-    base = torch.empty(1, O, I, dtype=torch.uint8, device=dev) if w.relaxation == "shift" else None
-    layer.get_state(logits=lg, scales=sc, base=base)
-    np.testing.assert_array_equal(sc.cpu().numpy()[:, rows], st.scales)
-    assert rel_err(lg.cpu().numpy()[:, rows], st.logits) <= 1e-6
-    if base is not None:
-        np.testing.assert_array_equal(base.cpu().numpy()[:, rows], st.base)
+    ix = np.ix_(experts, rows)
+    buf = torch.empty(Bn, O, I, K, device=dev)           # one state plane set at a time
+    sbuf = torch.empty(Bn, O, I // gs, device=dev)
+
+    def planes(**which):
+        ((key, out),) = which.items()
+        t = layer.get_state(**{key: out})
+        return out[experts][:, rows].cpu().numpy(), t
+
+    st = ref.init_layer(rcfg, W, rows=rows, batches=experts)
+    lg, _ = planes(logits=buf)
+    sc, _ = planes(scales=sbuf)
+    np.testing.assert_array_equal(sc, st.scales)
+    assert rel_err(lg, st.logits) <= 1e-6
+    if w.relaxation == "shift":
+        base = torch.empty(Bn, O, I, dtype=torch.uint8, device=dev)
+        layer.get_state(base=base)
+        np.testing.assert_array_equal(base[experts][:, rows].cpu().numpy(), st.base)
     T = w.steps
     for t in range(2):
         tau, nxt = ref.tau_schedule(t, T), ref.tau_schedule(t + 1, T)
-        prm = B.StepParams(tau=tau, tau_next=nxt)
-        loss = torch.zeros(1, device=dev)
+        prm = B.StepParams(tau=tau, tau_next=nxt, lr_scales=w.lr_scales)
+        loss = torch.zeros(Bn, device=dev)
         layer.step(prm, loss_out=loss)
-        G = torch.empty(1, O, I, device=dev)
+        G = torch.empty(Bn, O, I, device=dev)
         layer.intermediates(grad=G)
-        st_new, _, inter = ref.step(rcfg, W, Hs, st, oracle_params(prm), rows=rows, want=True)
-        assert rel_err(G.cpu().numpy()[:, rows], inter["G"]) <= 1e-3
-        got = {k: torch.empty(1, O, I, K, device=dev) for k in ("logits", "m", "v")}
-        got.update({k: torch.empty(1, O, I // gs, device=dev) for k in ("scales", "m_s", "v_s")})
-        tt = layer.get_state(**got)
-        gst = ref.State(*(got[k].cpu().numpy()[:, rows] for k in ("logits", "m", "v", "scales", "m_s", "v_s")), tt)
+        G_rows = G[experts][:, rows].cpu().numpy()
+        del G
+        st_new, _, inter = ref.step(rcfg, W, Hs, st, oracle_params(prm), rows=rows, want=True,
+                                    batches=experts)
+        assert rel_err(G_rows, inter["G"]) <= 1e-3, (t, rel_err(G_rows, inter["G"]))
+        got = {}
+        for key in ("logits", "m", "v"):
+            got[key], tt = planes(**{key: buf})
+        for key in ("scales", "m_s", "v_s"):
+            got[key], _ = planes(**{key: sbuf})
+        gst = ref.State(*(got[k] for k in ("logits", "m", "v", "scales", "m_s", "v_s")), tt)
         assert_state_close(gst, st_new, inter["G"], 1e-3, t + 1, label=f"{name} step {t}",
                            dlogits=inter["dlogits"])
-        assert np.isfinite(loss.item()) and loss.item() > 0
+        lv = loss.cpu().numpy()
+        assert np.all(np.isfinite(lv)) and np.all(lv > 0)
         st = st_new
     layer.destroy()
 
