@@ -96,7 +96,8 @@ void free_layer(gsq::Layer* L) {
   }
   for (hipEvent_t e : L->event_pool) (void)hipEventDestroy(e);
   void* bufs[] = {L->W, L->H, L->L, L->M, L->V, L->S, L->MS, L->VS, L->R[0], L->R[1],
-                  L->G, L->partials, L->loss_part, L->loss_stage, L->loss_tickets, L->flag, L->sb_d, L->sb_sc, L->codes,
+                  L->G, L->partials, L->loss_part, L->loss_stage, L->loss_tickets, L->split_ws,
+                  L->flag, L->sb_d, L->sb_sc, L->codes,
                   L->J0};
   for (void* p : bufs)
     if (p) (void)hipFree(p);
@@ -215,6 +216,13 @@ gsq_status gsq_layer_init(const gsq_config* cfg, const void* W, int32_t w_dtype,
   const size_t npad = (size_t)(L.B * L.Opad * L.Ipad);
   L.tiles_per_batch = gsq::contract_tiles_per_batch(L);
   L.loss_cols = (L.I + 255) / 256;
+  {
+    int dev = 0, ncu = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess)
+      gsq::plan_contract_split(L, ncu);
+    (void)hipGetLastError();
+  }
   bool ok = alloc(&L.W, L.N * (L.w_bf16 ? 2 : 4)) &&
             alloc(&L.H, (size_t)(L.B * L.Ipad * L.Ipad) * relem) &&
             alloc(&L.L, L.K * L.N * 4) && alloc(&L.M, L.K * L.N * 4) && alloc(&L.V, L.K * L.N * 4) &&
@@ -228,6 +236,7 @@ gsq_status gsq_layer_init(const gsq_config* cfg, const void* W, int32_t w_dtype,
   if (ok && cfg->layout == GSQ_LAYOUT_SUPERBLOCK)
     ok = alloc(&L.sb_d, (L.N / 256) * 2) && alloc(&L.sb_sc, L.N / 16);
   if (ok && cfg->relaxation == GSQ_RELAX_SHIFT) ok = alloc(&L.J0, (size_t)L.N);
+  if (ok && L.split_parts > 1) ok = alloc(&L.split_ws, (size_t)gsq::contract_split_ws_floats(L) * 4);
   if (!ok) {
     free_layer(h);
     return fail(GSQ_ENOMEM, "device allocation failed for a %lld x %lld x %lld layer",

@@ -38,13 +38,15 @@ __device__ __forceinline__ void block_sum_to(double x, double* out) {
   if (threadIdx.x == 0) *out = red[0];
 }
 
-// Tile of block `bid`.  Workgroups are handed to the 8 XCDs round-robin; renumbering so
-// each XCD owns a contiguous range, then sweeping GROUP_M tile rows at a time, keeps the
-// R and H panels a group shares in the same XCD's L2.
-__device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
-  const int nblk = tiles_m * tiles_n;
-  int lin = bid;
-  if ((nblk & 7) == 0) lin = (bid & 7) * (nblk >> 3) + (bid >> 3);
+// Position of block `bid` in the tile order.  Workgroups are handed to the 8 XCDs round-robin;
+// renumbering so each XCD owns a contiguous range of the nblk blocks keeps the R and H panels a
+// group of tiles shares in the same XCD's L2.
+__device__ __forceinline__ int lin_of(int bid, int nblk) {
+  return (nblk & 7) == 0 ? (bid & 7) * (nblk >> 3) + (bid >> 3) : bid;
+}
+
+// Tile at position `lin`: GROUP_M tile rows are swept together, column by column.
+__device__ __forceinline__ void tile_at(int lin, int tiles_m, int tiles_n, int& tm, int& tn) {
   const int per_group = GROUP_M * tiles_n;
   const int first_m = (lin / per_group) * GROUP_M;
   const int gsz = min(tiles_m - first_m, GROUP_M);
@@ -52,6 +54,16 @@ __device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& 
   tm = first_m + r % gsz;
   tn = r / gsz;
 }
+
+// Work of one launch.  The first `full` blocks compute whole tiles (positions 0 .. full - 1).
+// When the tiles do not fill a whole number of rounds of the GPU, the tiles of the last, partly
+// empty round (positions full ..) are split along K: block full + q computes part q % split of
+// tile full + q / split and writes its raw P to ws; k_contract_fixup adds the parts in order.
+struct Split {
+  int full;
+  int split;    // 1: no split
+  float* ws;    // (tiles - full) x split x 256 x 256 fp32
+};
 
 // One 256 x 256 tile of G per workgroup; four wavefronts each own 128 x 128 as 4 x 4 MFMA
 // 32x32x16 tiles.  K slabs 64 wide (whole 128-byte lines of R and H) stream through two LDS
@@ -105,14 +117,26 @@ __global__ __launch_bounds__(256, 1) void k_contract_bf16(const uint16_t* __rest
                                                           float* __restrict__ G,
                                                           double* __restrict__ partials,
                                                           int64_t Opad, int64_t Ipad, int tiles_m,
-                                                          int tiles_n, int want_loss) {
+                                                          int tiles_n, int want_loss, Split sp) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const int64_t b = blockIdx.z;
+  int nk = (int)(Ipad / BK);   // a multiple of 4 (Ipad is a multiple of 256)
+  int lin, part = -1, kb = 0;
+  if ((int)blockIdx.x < sp.full) {
+    lin = lin_of(blockIdx.x, sp.full);
+  } else {   // a K part of a tile of the last round (XCD-contiguous numbering as well)
+    const int nq = (int)gridDim.x - sp.full;
+    const int q = lin_of(blockIdx.x - sp.full, nq);
+    lin = sp.full + q / sp.split;
+    part = q % sp.split;
+    nk /= sp.split;
+    kb = part * nk;
+  }
   int tm, tn;
-  tile_of(blockIdx.x, tiles_m, tiles_n, tm, tn);
+  tile_at(lin, tiles_m, tiles_n, tm, tn);
   const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
-  const uint16_t* A = R + b * Opad * Ipad + m0 * Ipad;
-  const uint16_t* Bt = H + b * Ipad * Ipad + n0 * Ipad;
+  const uint16_t* A = R + b * Opad * Ipad + m0 * Ipad + (int64_t)kb * BK;
+  const uint16_t* Bt = H + b * Ipad * Ipad + n0 * Ipad + (int64_t)kb * BK;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
@@ -133,7 +157,6 @@ __global__ __launch_bounds__(256, 1) void k_contract_bf16(const uint16_t* __rest
     // < 256 Ipad + 64 <= 2^32 for the widest layer the library accepts (I <= 2^24)
     off[j] = (uint32_t)row * (uint32_t)Ipad + (uint32_t)(((lane & 7) ^ swz(row)) * 8);
   }
-  const int nk = (int)(Ipad / BK);   // a multiple of 4 (Ipad is a multiple of 256)
 #define GSQ_ISSUE(K)                                                                     \
   do {                                                                                   \
     uint8_t* st_ = smem + ((K) % STAGES) * 2 * SLAB_BYTES + wave * 64 * ROW_BYTES;       \
@@ -219,6 +242,18 @@ __global__ __launch_bounds__(256, 1) void k_contract_bf16(const uint16_t* __rest
 #undef GSQ_ISSUE
 
   // 32 x 32 accumulator layout: lane l, register r -> row 8*(r/4) + 4*(l/32) + r%4, column l%32
+  if (part >= 0) {   // raw P of this K part, tile-local row-major
+    float* W_ = sp.ws + ((int64_t)(lin - sp.full) * sp.split + part) * (BM * BN);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          W_[(wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * BN + wn * 128 + j * 32 +
+             (lane & 31)] = acc[i][j][r];
+    return;
+  }
   float* Gb = G + b * Opad * Ipad;
   const uint16_t* Rb = R + b * Opad * Ipad;
   double lsum = 0.0;
@@ -235,6 +270,27 @@ __global__ __launch_bounds__(256, 1) void k_contract_bf16(const uint16_t* __rest
         if (want_loss) lsum += (double)bf16_to_f32(Rb[row * Ipad + col]) * (double)p;
       }
   if (want_loss) block_sum_to(lsum, partials + b * (int64_t)tiles_m * tiles_n + tm * tiles_n + tn);
+}
+
+// G = -2 (P_0 + ... + P_{split-1}) for the split tiles of the last round, parts added in order.
+__global__ __launch_bounds__(256) void k_contract_fixup(const float* __restrict__ ws,
+                                                        float* __restrict__ G, int64_t Ipad,
+                                                        int tiles_m, int tiles_n, Split sp) {
+  const int q = blockIdx.x;
+  int tm, tn;
+  tile_at(sp.full + q, tiles_m, tiles_n, tm, tn);
+  const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
+  const float* src = ws + (int64_t)q * sp.split * (BM * BN);
+  for (int e = threadIdx.x * 4; e < BM * BN; e += 256 * 4) {
+    float4 acc = *reinterpret_cast<const float4*>(src + e);
+    for (int p = 1; p < sp.split; ++p) {
+      const float4 v = *reinterpret_cast<const float4*>(src + (int64_t)p * (BM * BN) + e);
+      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+    }
+    const int lr = e / BN, lc = e % BN;
+    *reinterpret_cast<float4*>(G + (m0 + lr) * Ipad + n0 + lc) =
+        make_float4(-2.f * acc.x, -2.f * acc.y, -2.f * acc.z, -2.f * acc.w);
+  }
 }
 
 // FP32 precision: 64 x 64 tile per workgroup, 4 x 4 outputs per thread, fp64 accumulation.
@@ -364,10 +420,19 @@ hipError_t launch_contract(const Layer& L, const void* R, bool want_loss, int sl
       attr_set = true;
     }
     const int tiles_m = (int)(L.Opad / BM), tiles_n = (int)(L.Ipad / BN);
-    dim3 grid((unsigned)(tiles_m * tiles_n), 1, (unsigned)L.B);
+    const int tiles = tiles_m * tiles_n;
+    Split sp{tiles, 1, nullptr};
+    if (L.split_parts > 1 && !want_loss) sp = Split{L.split_full, L.split_parts, L.split_ws};
+    dim3 grid((unsigned)(sp.full + (tiles - sp.full) * sp.split), 1, (unsigned)L.B);
     hipLaunchKernelGGL(k_contract_bf16, grid, dim3(256), LDS_BYTES, s,
                        static_cast<const uint16_t*>(R), static_cast<const uint16_t*>(L.H), G,
-                       partials, L.Opad, L.Ipad, tiles_m, tiles_n, want_loss ? 1 : 0);
+                       partials, L.Opad, L.Ipad, tiles_m, tiles_n, want_loss ? 1 : 0, sp);
+    if (sp.split > 1) {
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL(k_contract_fixup, dim3((unsigned)(tiles - sp.full)), dim3(256), 0, s,
+                         sp.ws, G, L.Ipad, tiles_m, tiles_n, sp);
+    }
   } else {
     dim3 grid((unsigned)(L.Ipad / TN), (unsigned)(L.Opad / TM), (unsigned)L.B);
     hipLaunchKernelGGL(k_contract_f32, grid, dim3(256), 0, s, static_cast<const float*>(R),
@@ -375,6 +440,29 @@ hipError_t launch_contract(const Layer& L, const void* R, bool want_loss, int sl
                        want_loss ? 1 : 0);
   }
   return hipGetLastError();
+}
+
+void plan_contract_split(Layer& L, int num_cu) {
+  L.split_full = 0;
+  L.split_parts = 1;
+  if (!L.bf16 || L.B != 1 || num_cu <= 0) return;
+  const int tiles = (int)((L.Opad / BM) * (L.Ipad / BN));
+  const int rest = tiles % num_cu;
+  if (tiles < num_cu || rest == 0 || rest > num_cu / 2) return;
+  const int nk = (int)(L.Ipad / BK);
+  if (nk < 128) return;   // short K loops: the partial-product traffic would cost more than it saves
+  int split = 1;
+  for (int s = 2; s <= 4; s *= 2)
+    if (rest * s <= num_cu && nk % s == 0 && nk / s >= 2) split = s;
+  if (split == 1) return;
+  L.split_full = tiles - rest;
+  L.split_parts = split;
+}
+
+int64_t contract_split_ws_floats(const Layer& L) {
+  if (L.split_parts <= 1) return 0;
+  const int tiles = (int)((L.Opad / BM) * (L.Ipad / BN));
+  return (int64_t)(tiles - L.split_full) * L.split_parts * BM * BN;
 }
 
 int64_t loss_stage_size(const Layer& L) {

@@ -71,6 +71,9 @@ struct Layer {
   int sample_slots = 1;        // capacity of G in samples
   int last_sample = 0;         // slot holding the most recent step's last sample
   int64_t tiles_per_batch = 0;
+  // contraction work split of a partly empty last round (see plan_contract_split)
+  int split_full = 0, split_parts = 1;
+  float* split_ws = nullptr;
   int* flag = nullptr;
   uint16_t* sb_d = nullptr;
   uint8_t* sb_sc = nullptr;
@@ -111,6 +114,11 @@ ElemArgs base_args(const Layer& L);
 // ---- launchers (gsq_contract.hip)
 int64_t contract_tiles_per_batch(const Layer& L);
 int64_t loss_stage_size(const Layer& L);   // doubles
+// Split the K range of the tiles of a last, at most half-full round of the GPU's num_cu
+// compute units over 2 or 4 blocks each (BF16 precision, one layer, at least 128 K slabs per
+// tile); sets split_full/_parts.
+void plan_contract_split(Layer& L, int num_cu);
+int64_t contract_split_ws_floats(const Layer& L);
 hipError_t launch_contract(const Layer& L, const void* R, bool want_loss, int slot, hipStream_t s);
 // Loss of each layer from the contraction's tile partials (slot 0) or, with from_rows, from the
 // backward's row partials, times `scale`.

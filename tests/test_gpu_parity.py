@@ -458,3 +458,26 @@ def test_samples_out_of_range_rejected(dev):
     pair = Pair(rcfg, W, H, dev)
     with pytest.raises(RuntimeError, match="samples"):
         pair.step(B.StepParams(tau=0.5, samples=B.MAX_SAMPLES + 1))
+
+
+def test_optimiser_switch_keeps_the_state(dev):
+    """Four Adam steps, four Lion steps, four Adam steps: Lion leaves the second moment alone, so
+    the later Adam steps continue from the earlier moments."""
+    w = inputs.WORKLOADS["tiny-256x256-k4"]
+    W, H = inputs.make_layer(w)
+    rcfg = ref.Config(256, 256, w.levels, 128, precision="fp32", seed=3)
+    pair = Pair(rcfg, W, H, dev)
+    st = ref.init_layer(rcfg, W)
+    T = 12
+    for t in range(T):
+        lion = 4 <= t < 8
+        prm = B.StepParams(tau=ref.tau_schedule(t, T), lr_logits=1e-3 if lion else 1e-2,
+                           optimizer=B.OPT_LION if lion else B.OPT_ADAM,
+                           tau_next=ref.tau_schedule(t + 1, T) if t + 1 < T else 0.0)
+        lg = pair.step(prm)[0]
+        st, L = ref.step(rcfg, W, pair.Hs, st, oracle_params(prm))
+        assert abs(lg - L[0]) <= 1e-5 * abs(L[0]), (t, lg, L[0])
+        if t in (3, 7, 11):
+            got = pair.get()
+            for k in ("logits", "m", "v", "scales"):
+                assert rel_err(getattr(got, k), getattr(st, k)) <= 1e-5, (t, k)
