@@ -221,11 +221,11 @@ gsq_status gsq_gumbel(const gsq_config* cfg, int64_t e0, int64_t count, int64_t 
 enum {
   GSQ_KERNEL_INIT = 0,      /* H symmetrisation, scale and logit initialisation        */
   GSQ_KERNEL_FORWARD = 1,   /* the sample of Alg. 1 and the residual R                 */
-  GSQ_KERNEL_CONTRACT = 2,  /* P = R H, G = -2 P, loss partials                         */
+  GSQ_KERNEL_CONTRACT = 2,  /* P = R H, G = -2 P (hard loss: + loss partials)           */
   GSQ_KERNEL_REDUCE = 3,    /* loss partials -> loss                                    */
-  GSQ_KERNEL_BACKWARD = 4,  /* gradient + Adam (+ the next step's sample)               */
-  GSQ_KERNEL_HARDEN = 5,    /* argmax, effective scales, hard residual                  */
-  GSQ_KERNEL_PACK = 6,      /* bitstream / super-block packing                          */
+  GSQ_KERNEL_BACKWARD = 4,  /* gradient + optimiser + loss terms (+ the next sample)    */
+  GSQ_KERNEL_HARDEN = 5,    /* codes, effective scales, hard residual                   */
+  GSQ_KERNEL_PACK = 6,      /* bitstream / base-3 / super-block packing                 */
   GSQ_NUM_KERNELS = 7
 };
 

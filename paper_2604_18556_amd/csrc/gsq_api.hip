@@ -119,19 +119,22 @@ bool alloc(T** p, size_t bytes) {
 constexpr size_t kMaxPending = 8192;
 
 hipError_t harvest(gsq::Layer& L) {
-  for (auto& p : L.pending) {
-    hipError_t e = hipEventSynchronize(p.second.second);
-    if (e != hipSuccess) return e;
+  size_t done = 0;
+  hipError_t e = hipSuccess;
+  for (; done < L.pending.size(); ++done) {
+    auto& p = L.pending[done];
+    e = hipEventSynchronize(p.second.second);
     float ms = 0.f;
-    e = hipEventElapsedTime(&ms, p.second.first, p.second.second);
-    if (e != hipSuccess) return e;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, p.second.first, p.second.second);
+    if (e != hipSuccess) break;
     L.timed_ms[p.first] += ms;
     L.timed_launches[p.first] += 1;
     L.event_pool.push_back(p.second.first);
     L.event_pool.push_back(p.second.second);
   }
-  L.pending.clear();
-  return hipSuccess;
+  // only the pairs that were read go back to the pool
+  L.pending.erase(L.pending.begin(), L.pending.begin() + done);
+  return e;
 }
 
 hipError_t take_event(gsq::Layer& L, hipEvent_t* e) {
@@ -223,6 +226,14 @@ gsq_status gsq_layer_init(const gsq_config* cfg, const void* W, int32_t w_dtype,
       gsq::plan_contract_split(L, ncu);
     (void)hipGetLastError();
   }
+  if (L.bf16) {
+    // the contraction's LDS ring exceeds the default limit (set on the current device)
+    const hipError_t e = gsq::prepare_contract_kernel();
+    if (e != hipSuccess) {
+      delete h;
+      return hip_fail(e, "hipFuncSetAttribute");
+    }
+  }
   bool ok = alloc(&L.W, L.N * (L.w_bf16 ? 2 : 4)) &&
             alloc(&L.H, (size_t)(L.B * L.Ipad * L.Ipad) * relem) &&
             alloc(&L.L, L.K * L.N * 4) && alloc(&L.M, L.K * L.N * 4) && alloc(&L.V, L.K * L.N * 4) &&
@@ -278,7 +289,11 @@ static gsq_status grow_sample_slots(gsq::Layer& L, int M) {
   const size_t npad = (size_t)(L.B * L.Opad * L.Ipad);
   float* G = nullptr;
   if (!alloc(&G, (size_t)M * npad * 4)) return fail(GSQ_ENOMEM, "no room for %d samples", M);
-  GSQ_HIP(hipDeviceSynchronize());   // no launch on any stream still reads the old buffer
+  const hipError_t e = hipDeviceSynchronize();   // no launch on any stream still reads the old one
+  if (e != hipSuccess) {
+    (void)hipFree(G);
+    return hip_fail(e, "hipDeviceSynchronize");
+  }
   (void)hipFree(L.G);
   L.G = G;
   L.sample_slots = M;
@@ -331,6 +346,9 @@ gsq_status gsq_step(gsq_layer* h, const gsq_step_params* p, float* loss_out, hip
 
   const bool have = L.r_valid && L.r_t == L.t && L.r_tau == p->tau && L.r_kappa == p->kappa &&
                     L.r_noise == a.noise;
+  // until this step has been enqueued completely, no prepared sample or intermediate is claimed
+  L.r_valid = false;
+  L.last = -1;
   const int use = L.cur;
   a.Rout = L.R[use];
   for (int smp = 0; smp < M; ++smp) {

@@ -404,6 +404,11 @@ __global__ void k_reduce_loss(const double* partials, int64_t per_batch, int nch
 
 }  // namespace
 
+hipError_t prepare_contract_kernel() {
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(k_contract_bf16),
+                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)LDS_BYTES);
+}
+
 int64_t contract_tiles_per_batch(const Layer& L) {
   return L.bf16 ? (L.Opad / BM) * (L.Ipad / BN) : (L.Opad / TM) * (L.Ipad / TN);
 }
@@ -412,13 +417,6 @@ hipError_t launch_contract(const Layer& L, const void* R, bool want_loss, int sl
   float* G = L.G + (int64_t)slot * L.B * L.Opad * L.Ipad;
   double* partials = L.partials;
   if (L.bf16) {
-    static bool attr_set = false;
-    if (!attr_set) {
-      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k_contract_bf16),
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)LDS_BYTES);
-      if (e != hipSuccess) return e;
-      attr_set = true;
-    }
     const int tiles_m = (int)(L.Opad / BM), tiles_n = (int)(L.Ipad / BN);
     const int tiles = tiles_m * tiles_n;
     Split sp{tiles, 1, nullptr};
