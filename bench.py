@@ -61,6 +61,18 @@ def algorithmic_work(w, fused, want_loss, lr_scales, lion=False, samples=1):
     return {"forward": ("hbm", fwd), "backward": ("hbm", bwd), "contract": ("flops", flops, contract_bytes)}
 
 
+def harden_bytes(w, hard_loss):
+    """Algorithmic bytes of gsq_harden: the K logit planes, the shift's base index, one code byte,
+    and with a hard loss W and the hard residual; plus the scales read and the fp16 scales
+    written (4 + 4 bytes per group)."""
+    K = {"shift": 5, "ternary": 2}.get(w.relaxation, len(w.levels))
+    gs = 16 if w.layout == "superblock" else w.group_size
+    n = w.batch * w.out_features * w.in_features
+    wb = 2 if w.precision == "bf16" else 4
+    per = 4 * K + (1 if w.relaxation == "shift" else 0) + 1 + (2 * wb if hard_loss else 0)
+    return n * per + n // gs * 8
+
+
 def source_sha(path):
     with open(path, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()
@@ -225,8 +237,9 @@ def main():
     packed = torch.empty(B.packed_size(cfg), dtype=torch.uint8, device=dev)
     layer.timing(True)
     layer.harden(codes=codes, hard_loss=hl)
-    layer.pack(packed)
     once = layer.timing_read(reset=True)
+    layer.pack(packed)
+    once_pack = layer.timing_read(reset=True)
     layer.timing(False)
 
     work = algorithmic_work(w, fused, args.loss_every == 1, w.lr_scales, lion, args.samples)
@@ -252,6 +265,18 @@ def main():
     roofline = {"bound": d["bound"], "achieved": d["achieved"], "peak": d["peak"], "unit": d["unit"],
                 "frac": d["frac"], "traffic": measured_traffic(dom, w.name), "kernel": dom,
                 "avg_ms": d["avg_ms"], "source": src}
+
+    # the step's ideal time: each kernel's algorithmic bytes at the HBM peak, or flops at the
+    # matrix-core peak, added (the kernels run one after another)
+    ideal_ms = 0.0
+    for name, entry in per_kernel.items():
+        if entry.get("unit") == "GB/s":
+            ideal_ms += entry["ms_per_step"] / entry["avg_ms"] * entry["bytes_per_launch"] / (PEAK_HBM_GBS * 1e9) * 1e3
+        elif entry.get("unit") == "TFLOP/s":
+            ideal_ms += entry["ms_per_step"] / entry["avg_ms"] * entry["flops_per_launch"] / (entry["peak"] * 1e12) * 1e3
+    h_ms = once["harden"][0]
+    h_bytes = harden_bytes(w, hard_loss=True)
+    p_ms = once_pack["pack"][0]
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -285,9 +310,17 @@ def main():
         "kernels": per_kernel,
         "kernel_timing_pass": {"steps": args.steps, "wall_ms": ms_timed_pass,
                                "note": "per-kernel HIP events; throughput is timed without them"},
+        "step_roofline": {"ideal_ms": ideal_ms, "frac": ideal_ms / ms_step,
+                          "note": "sum over the step's kernels of algorithmic bytes / 8 TB/s and "
+                                  "flops / matrix-core peak, over the measured step time"},
         "once_per_layer": {"init_ms": init_ms,
-                           "harden_ms": once["harden"][0], "pack_ms": once["pack"][0],
-                           "hard_loss_contract_ms": once["contract"][0]},
+                           "harden_ms": h_ms, "harden_bytes": h_bytes,
+                           "harden_GBps": h_bytes / (h_ms * 1e-3) / 1e9 if h_ms > 0 else None,
+                           "pack_ms": p_ms, "pack_harden_ms": once_pack["harden"][0],
+                           "hard_loss_contract_ms": once["contract"][0],
+                           "note": "harden: codes, hard residual and fp16 scales (gsq_harden with "
+                                   "a hard loss); pack: the bit-packing kernels of gsq_pack, which "
+                                   "first re-derives the codes (pack_harden_ms)"},
         "gpu_vs_cpu": None if cpu is None else (1e3 / ms_step) / cpu["value"],
     }
     print(json.dumps(out), flush=True)

@@ -605,39 +605,67 @@ __global__ void k_init_logits(const void* W, int w_bf16, const float* S, float* 
 // delta* the argmax shift; TERNARY: Alg. 2's thresholds, active iff l_m >= 0, positive iff
 // l_b >= 0, q = 1 + mask * sign.  Optionally the hard residual R = W - s c[q] (s rounded to
 // fp16 in the group layouts) written in the contraction's padded layout, fp32 when
-// r_f32 != 0, bf16 otherwise.
-__global__ void k_harden(ElemArgs a, int K, int relax, int superblock, int r_f32, uint8_t* codes,
-                         void* Rh) {
-  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < a.N;
-       e += (int64_t)gridDim.x * blockDim.x) {
-    int q = 0;
+// r_f32 != 0, bf16 otherwise.  Rows and columns as in the forward: four rows per block, four
+// consecutive columns per lane (I is a multiple of 16, so a lane's columns share a group).
+__global__ __launch_bounds__(kBlock) void k_harden(ElemArgs a, int K, int relax, int superblock,
+                                                   int r_f32, uint8_t* codes, void* Rh) {
+  const int lane = threadIdx.x & 63;
+  const int64_t col0 = (int64_t)blockIdx.x * kCols + lane * 4;
+  const int64_t gpr = a.I / a.gs;
+  const bool codes4 = (reinterpret_cast<uintptr_t>(codes) & 3) == 0;
+  for (int64_t row = (int64_t)blockIdx.y * 4 + (threadIdx.x >> 6); row < a.rows;
+       row += (int64_t)gridDim.y * 4) {
+    if (col0 >= a.I) continue;
+    const int64_t e0 = row * a.I + col0;
+    int q[4] = {0, 0, 0, 0};
     if (relax == GSQ_RELAX_TERNARY) {
-      const bool active = a.L[e] >= 0.f, positive = a.L[a.N + e] >= 0.f;
-      q = active ? (positive ? 2 : 0) : 1;
+      const float4 mask = *reinterpret_cast<const float4*>(a.L + e0);
+      const float4 sign = *reinterpret_cast<const float4*>(a.L + a.N + e0);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        q[j] = f4get(mask, j) >= 0.f ? (f4get(sign, j) >= 0.f ? 2 : 0) : 1;
     } else {
-      float best = a.L[e];
+      float4 best = *reinterpret_cast<const float4*>(a.L + e0);
       for (int k = 1; k < K; ++k) {
-        const float x = a.L[k * a.N + e];
-        if (x > best) { best = x; q = k; }
+        const float4 x = *reinterpret_cast<const float4*>(a.L + k * a.N + e0);
+        if (x.x > best.x) { best.x = x.x; q[0] = k; }
+        if (x.y > best.y) { best.y = x.y; q[1] = k; }
+        if (x.z > best.z) { best.z = x.z; q[2] = k; }
+        if (x.w > best.w) { best.w = x.w; q[3] = k; }
       }
       if (relax == GSQ_RELAX_SHIFT) {
-        int j = a.J0[e];
-        j = j < a.n_grid ? j : a.n_grid - 1;
-        q = j + q - 2;
-        q = q < 0 ? 0 : (q > a.n_grid - 1 ? a.n_grid - 1 : q);
+        const uint32_t j4 = *reinterpret_cast<const uint32_t*>(a.J0 + e0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          int b = (int)((j4 >> (8 * j)) & 0xFFu);
+          b = b < a.n_grid ? b : a.n_grid - 1;
+          const int c = b + q[j] - 2;
+          q[j] = c < 0 ? 0 : (c > a.n_grid - 1 ? a.n_grid - 1 : c);
+        }
       }
     }
-    if (codes) codes[e] = (uint8_t)q;
+    if (codes) {
+      if (codes4) {
+        *reinterpret_cast<uint32_t*>(codes + e0) =
+            (uint32_t)q[0] | ((uint32_t)q[1] << 8) | ((uint32_t)q[2] << 16) | ((uint32_t)q[3] << 24);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) codes[e0 + j] = (uint8_t)q[j];
+      }
+    }
     if (Rh) {
-      float s = a.S[e / a.gs];
+      float s = a.S[row * gpr + col0 / a.gs];
       if (!superblock) s = __half2float(__float2half_rn(s));
-      float cq = a.c[0];
-      for (int k = 1; k < GSQ_MAX_LEVELS; ++k) if (k == q) cq = a.c[k];
-      const float r = load_w1(a.W, a.w_bf16, e) - s * cq;
-      const int64_t row = e / a.I;
-      const int64_t idx = padded_index(a, row, e - row * a.I);
-      if (r_f32) static_cast<float*>(Rh)[idx] = r;
-      else static_cast<uint16_t*>(Rh)[idx] = bf16_rne(r);
+      float w[4], r[4];
+      load_w4(a.W, a.w_bf16, e0, w);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        float cq = a.c[0];
+        for (int k = 1; k < GSQ_MAX_LEVELS; ++k) if (k == q[j]) cq = a.c[k];
+        r[j] = w[j] - s * cq;
+      }
+      if (r_f32) store_r4<true>(Rh, padded_index(a, row, col0), r);
+      else store_r4<false>(Rh, padded_index(a, row, col0), r);
     }
   }
 }
@@ -888,7 +916,7 @@ hipError_t launch_backward(const Layer& L, const ElemArgs& a, bool update_scales
 
 hipError_t launch_harden(const Layer& L, uint8_t* codes, void* Rh, hipStream_t s) {
   const ElemArgs a = base_args(L);
-  hipLaunchKernelGGL(k_harden, flat_grid(L.N), dim3(256), 0, s, a, (int)L.K, L.relax,
+  hipLaunchKernelGGL(k_harden, row_grid(L), dim3(kBlock), 0, s, a, (int)L.K, L.relax,
                      L.cfg.layout == GSQ_LAYOUT_SUPERBLOCK ? 1 : 0, L.bf16 ? 0 : 1, codes, Rh);
   return hipGetLastError();
 }
