@@ -20,18 +20,21 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int BM = kTileM, BN = kTileN, BK = 64;
-constexpr int STAGES = 2;                                // LDS ring of K slabs
+constexpr int A_STAGES = 3;                              // LDS ring of R's K slabs
+constexpr int B_STAGES = 2;                              // LDS ring of H's K slabs
 constexpr int ROW_BYTES = BK * 2;                        // one 64-wide bf16 row: a full cache line
-constexpr int SLAB_BYTES = BM * ROW_BYTES;               // 32 KB per operand per stage
-constexpr size_t LDS_BYTES = (size_t)STAGES * 2 * SLAB_BYTES;
-constexpr int LOADS_PER_STAGE = 2 * SLAB_BYTES / 1024 / 4;   // 1 KB loads per wavefront per stage
+constexpr int SLAB_BYTES = BM * ROW_BYTES;               // 32 KB per operand slab
+constexpr int B_BASE = A_STAGES * SLAB_BYTES;            // H's ring after R's
+constexpr size_t LDS_BYTES = (size_t)(A_STAGES + B_STAGES) * SLAB_BYTES;   // 160 KB
+constexpr int LOADS_PER_OPERAND = SLAB_BYTES / 1024 / 4;   // 1 KB loads per wavefront per operand slab
 constexpr int GROUP_M = 8;           // tile rows swept together for L2 reuse
 
-__device__ __forceinline__ void block_sum_to(double x, double* out) {
-  __shared__ double red[256];
+// Sum over the workgroup into *out, through `red` (blockDim.x doubles of LDS, free to reuse).
+__device__ __forceinline__ void block_sum_to(double x, double* out, double* red) {
+  __syncthreads();
   red[threadIdx.x] = x;
   __syncthreads();
-  for (int w = 128; w > 0; w >>= 1) {
+  for (int w = blockDim.x / 2; w > 0; w >>= 1) {
     if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
     __syncthreads();
   }
@@ -66,10 +69,13 @@ struct Split {
 };
 
 // One 256 x 256 tile of G per workgroup; four wavefronts each own 128 x 128 as 4 x 4 MFMA
-// 32x32x16 tiles.  K slabs 64 wide (whole 128-byte lines of R and H) stream through two LDS
-// buffers by direct global->LDS loads (16 bytes per lane, no staging registers).  The steady-
-// state loop has no branches, so the fragment reads and slab loads are spread between the
-// matrix-core instructions (scheduling groups) instead of stalling them.
+// 32x32x16 tiles.  K slabs 64 wide (whole 128-byte lines of R and H) move by direct global->LDS
+// loads (16 bytes per lane, no staging registers) into a ring of three buffers for R and two for
+// H, the whole 160 KB of LDS.  R's third buffer lets its slab k + 2 be loaded during the first
+// half of slab k, H's during the second: the loads split evenly between the halves and R's get
+// one and a half slabs of time to land.  The steady-state loop has no branches, so the fragment
+// reads and slab loads are spread between the matrix-core instructions (scheduling groups)
+// instead of stalling them.
 //
 // LDS layout of a slab: row r occupies 128 bytes as eight 16-byte chunks, chunk c stored at
 // position c ^ f(r), f(r) = (r ^ (r >> 3)) & 7.  The fragment reads (consecutive rows, one
@@ -157,20 +163,19 @@ __global__ __launch_bounds__(256, 1) void k_contract_bf16(const uint16_t* __rest
     // < 256 Ipad + 64 <= 2^32 for the widest layer the library accepts (I <= 2^24)
     off[j] = (uint32_t)row * (uint32_t)Ipad + (uint32_t)(((lane & 7) ^ swz(row)) * 8);
   }
-#define GSQ_ISSUE(K)                                                                     \
-  do {                                                                                   \
-    uint8_t* st_ = smem + ((K) % STAGES) * 2 * SLAB_BYTES + wave * 64 * ROW_BYTES;       \
-    load_slab(A + (int64_t)(K) * BK, off, st_);                                          \
-    load_slab(Bt + (int64_t)(K) * BK, off, st_ + SLAB_BYTES);                            \
-  } while (0)
+#define GSQ_ISSUE_A(K) \
+  load_slab(A + (int64_t)(K) * BK, off, smem + ((K) % A_STAGES) * SLAB_BYTES + wave * 64 * ROW_BYTES)
+#define GSQ_ISSUE_B(K)                                                                   \
+  load_slab(Bt + (int64_t)(K) * BK, off,                                                 \
+            smem + B_BASE + ((K) % B_STAGES) * SLAB_BYTES + wave * 64 * ROW_BYTES)
   const int frow_a = wm * 128 + (lane & 31), frow_b = wn * 128 + (lane & 31);
   const int fchunk = lane >> 5;
 
 // fragments of sub-steps 2 HALF and 2 HALF + 1 of slab K into register set S
 #define GSQ_READ(S, K, HALF)                                                             \
   do {                                                                                   \
-    const uint8_t* As_ = smem + ((K) % STAGES) * 2 * SLAB_BYTES;                         \
-    const uint8_t* Bs_ = As_ + SLAB_BYTES;                                               \
+    const uint8_t* As_ = smem + ((K) % A_STAGES) * SLAB_BYTES;                           \
+    const uint8_t* Bs_ = smem + B_BASE + ((K) % B_STAGES) * SLAB_BYTES;                  \
     _Pragma("unroll") for (int h = 0; h < 2; ++h)                                        \
       _Pragma("unroll") for (int i = 0; i < 4; ++i) {                                    \
         const int c_ = (2 * (HALF) + h) * 2 + fchunk;                                    \
@@ -183,44 +188,42 @@ __global__ __launch_bounds__(256, 1) void k_contract_bf16(const uint16_t* __rest
     _Pragma("unroll") for (int i = 0; i < 4; ++i)                                        \
       _Pragma("unroll") for (int j = 0; j < 4; ++j)                                      \
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(S##a[h][i], S##b[h][j], acc[i][j], 0, 0, 0)
-// interleave: 16 x (one MFMA, one LDS read), then 16 MFMAs
-#define GSQ_SCHED_READS()                                                                \
-  _Pragma("unroll") for (int i_ = 0; i_ < 16; ++i_) {                                    \
-    __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);                                 \
-    __builtin_amdgcn_sched_group_barrier(SG_DSR, 1, 0);                                  \
-  }                                                                                      \
-  __builtin_amdgcn_sched_group_barrier(SG_MFMA, 16, 0)
-// interleave: 16 x (one MFMA, one LDS read), then 16 x (one MFMA, one global->LDS load): the
-// next slab's fragments arrive early, the loads have a whole slab of time to land
+// interleave: 16 x (one MFMA, one LDS read), then 8 x (one MFMA, one global->LDS load) and 8
+// MFMAs
 #define GSQ_SCHED_LOADS_READS()                                                          \
   _Pragma("unroll") for (int i_ = 0; i_ < 16; ++i_) {                                    \
     __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);                                 \
     __builtin_amdgcn_sched_group_barrier(SG_DSR, 1, 0);                                  \
   }                                                                                      \
-  _Pragma("unroll") for (int i_ = 0; i_ < 16; ++i_) {                                    \
+  _Pragma("unroll") for (int i_ = 0; i_ < 8; ++i_) {                                     \
     __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);                                 \
     __builtin_amdgcn_sched_group_barrier(SG_VMEM, 1, 0);                                 \
-  }
+  }                                                                                      \
+  __builtin_amdgcn_sched_group_barrier(SG_MFMA, 8, 0)
 
   // p: first half (sub-steps 0, 1) of the current slab; q: second half (sub-steps 2, 3)
   bf16x8 pa[2][4], pb[2][4], qa[2][4], qb[2][4];
-  GSQ_ISSUE(0);
-  GSQ_ISSUE(1);
-  wait_vm<LOADS_PER_STAGE>();
+  GSQ_ISSUE_A(0);
+  GSQ_ISSUE_B(0);
+  GSQ_ISSUE_A(1);
+  GSQ_ISSUE_B(1);
+  wait_vm<2 * LOADS_PER_OPERAND>();
   slab_barrier();
   GSQ_READ(p, 0, 0);
-  // steady state: no branches, so loads and reads interleave with the matrix-core work
+  // steady state: R's slab kt + 2 is loaded during the first half of slab kt (its buffer last
+  // held slab kt - 1), H's during the second half (its buffer held slab kt, read by then)
   for (int kt = 0; kt < nk - 2; ++kt) {
     GSQ_READ(q, kt, 1);
+    GSQ_ISSUE_A(kt + 2);
     GSQ_MFMA(p);
-    GSQ_SCHED_READS();
+    GSQ_SCHED_LOADS_READS();
     __builtin_amdgcn_sched_barrier(0);   // every MFMA of this half is issued before the wait
-    // slab kt+1 (issued one slab ago) has landed, and every wavefront has read slab kt, whose
-    // buffer is then refilled with slab kt+2
-    wait_vm<0>();
+    // slab kt+1 has landed (only R's slab kt+2 may be in flight), and every wavefront has read
+    // slab kt
+    wait_vm<LOADS_PER_OPERAND>();
     slab_barrier();
     GSQ_READ(p, kt + 1, 0);
-    GSQ_ISSUE(kt + 2);
+    GSQ_ISSUE_B(kt + 2);
     GSQ_MFMA(q);
     GSQ_SCHED_LOADS_READS();
     __builtin_amdgcn_sched_barrier(0);
@@ -236,10 +239,10 @@ __global__ __launch_bounds__(256, 1) void k_contract_bf16(const uint16_t* __rest
   GSQ_MFMA(p);
   GSQ_MFMA(q);
 #undef GSQ_SCHED_LOADS_READS
-#undef GSQ_SCHED_READS
 #undef GSQ_MFMA
 #undef GSQ_READ
-#undef GSQ_ISSUE
+#undef GSQ_ISSUE_A
+#undef GSQ_ISSUE_B
 
   // 32 x 32 accumulator layout: lane l, register r -> row 8*(r/4) + 4*(l/32) + r%4, column l%32
   if (part >= 0) {   // raw P of this K part, tile-local row-major
@@ -269,7 +272,9 @@ __global__ __launch_bounds__(256, 1) void k_contract_bf16(const uint16_t* __rest
         Gb[row * Ipad + col] = -2.f * p;
         if (want_loss) lsum += (double)bf16_to_f32(Rb[row * Ipad + col]) * (double)p;
       }
-  if (want_loss) block_sum_to(lsum, partials + b * (int64_t)tiles_m * tiles_n + tm * tiles_n + tn);
+  if (want_loss)
+    block_sum_to(lsum, partials + b * (int64_t)tiles_m * tiles_n + tm * tiles_n + tn,
+                 reinterpret_cast<double*>(smem));
 }
 
 // G = -2 (P_0 + ... + P_{split-1}) for the split tiles of the last round, parts added in order.
@@ -345,7 +350,10 @@ __global__ __launch_bounds__(256) void k_contract_f32(const float* __restrict__ 
       if (want_loss) lsum += (double)Rb[row * Ipad + col] * acc[i][j];
     }
   if (want_loss)
-    block_sum_to(lsum, partials + (b * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x);
+  {
+    __shared__ double red[256];
+    block_sum_to(lsum, partials + (b * gridDim.y + blockIdx.y) * gridDim.x + blockIdx.x, red);
+  }
 }
 
 // Loss of layer b = scale * the sum of its per_batch partials, in a fixed order, in one launch:
