@@ -27,8 +27,14 @@ using Real = typename std::conditional<kF64, double, float>::type;
 __device__ __forceinline__ float f4get(const float4& v, int q) {
   return q == 0 ? v.x : q == 1 ? v.y : q == 2 ? v.z : v.w;
 }
+
 __device__ __forceinline__ void f4set(float4& v, int q, float x) {
   if (q == 0) v.x = x; else if (q == 1) v.y = x; else if (q == 2) v.z = x; else v.w = x;
+}
+
+__device__ __forceinline__ bool finite4(const float4& v) {
+  return __builtin_isfinite(v.x) && __builtin_isfinite(v.y) && __builtin_isfinite(v.z) &&
+         __builtin_isfinite(v.w);
 }
 
 __device__ __forceinline__ void load_w4(const void* W, int w_bf16, int64_t e, float (&w)[4]) {
@@ -322,8 +328,26 @@ __device__ __forceinline__ double wave_sum_to_lane63(double x) {
 // the updated logits and scale and its residual written to a.Rout.  With a.want_loss, the
 // loss terms R * P = R * (-G / 2) of this step's sample(s) are summed per row and 256-column
 // block (R rebuilt exactly as the contraction saw it) into a.loss_part.
+// Register budget of the backward.  Updating the moments one logit plane at a time (each
+// plane's m and v loaded just before its update) keeps 8K fewer registers live than loading
+// them all first, at the price of less memory parallelism within a wavefront.  It pays only
+// where it buys another wavefront per SIMD: the shift relaxation (2 -> 3 wavefronts, 5 % faster
+// at 4096 x 14336), grids of 5 to 7 levels (2 -> 3), and the 8-level grid with frozen scales
+// under a bound of three wavefronts in the one-sample bf16 path (2 % faster on the super-block
+// MoE).  With trained scales the 8-level grid would spill under that bound (3 % slower); it and
+// the smaller grids keep all moments in flight at once.
+template <int K, bool kScales, int kMode>
+constexpr bool backward_plane_update() {
+  return kMode == GSQ_RELAX_SHIFT || (kMode == GSQ_RELAX_GRID && K >= 5 && !(K == 8 && kScales));
+}
 template <int K, bool kF64, bool kScales, bool kMulti, int kMode>
-__global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
+constexpr int backward_min_blocks() {
+  return (kMode == GSQ_RELAX_GRID && K == 8 && !kScales && !kF64 && !kMulti) ? 3 : 1;
+}
+
+template <int K, bool kF64, bool kScales, bool kMulti, int kMode>
+__global__ __launch_bounds__(kBlock, (backward_min_blocks<K, kF64, kScales, kMulti, kMode>())) void k_backward(
+    ElemArgs a) {
   using T = Real<kF64>;
   constexpr int Z = noise_count<K, kMode>();
   __shared__ __align__(16) float win[kMode == GSQ_RELAX_SHIFT ? GSQ_MAX_LEVELS * kWinRow : 4];
@@ -348,7 +372,7 @@ __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
     const int64_t sidx = row * gpr + (active ? col0 / a.gs : 0);
     const float s32 = a.S[sidx];
     const T s = (T)s32;
-    float4 lv[K], mv[K], vv[K];
+    float4 lv[K];
     const int64_t gidx = active ? padded_index(a, row, col0) : 0;
 #pragma unroll
     for (int k = 0; k < K; ++k)
@@ -406,33 +430,57 @@ __global__ __launch_bounds__(kBlock) void k_backward(ElemArgs a) {
     }
     // the moments are needed only by the update: loading them here keeps them out of the
     // registers of the sample loop
-#pragma unroll
-    for (int k = 0; k < K; ++k) {
-      mv[k] = active ? *reinterpret_cast<const float4*>(a.M + k * a.N + e0)
-                     : make_float4(0.f, 0.f, 0.f, 0.f);
-      vv[k] = (active && !lion) ? *reinterpret_cast<const float4*>(a.V + k * a.N + e0)
-                                : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
+    if constexpr (backward_plane_update<K, kScales, kMode>()) {
 #pragma unroll
       for (int k = 0; k < K; ++k) {
-        T th = (T)f4get(lv[k], q), m1 = (T)f4get(mv[k], q), v1 = (T)f4get(vv[k], q);
-        opt_update<kF64>(lion, dacc[q][k], th, m1, v1, lr, step_l, b1, b2, omb1, omb2, rbc2, eps, wd);
-        f4set(mv[k], q, (float)m1);
-        f4set(vv[k], q, (float)v1);
-        f4set(lv[k], q, (float)th);
+        float4 mk = active ? *reinterpret_cast<const float4*>(a.M + k * a.N + e0)
+                           : make_float4(0.f, 0.f, 0.f, 0.f);
+        float4 vk = (active && !lion) ? *reinterpret_cast<const float4*>(a.V + k * a.N + e0)
+                                      : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          T th = (T)f4get(lv[k], q), m1 = (T)f4get(mk, q), v1 = (T)f4get(vk, q);
+          opt_update<kF64>(lion, dacc[q][k], th, m1, v1, lr, step_l, b1, b2, omb1, omb2, rbc2,
+                           eps, wd);
+          f4set(mk, q, (float)m1);
+          f4set(vk, q, (float)v1);
+          f4set(lv[k], q, (float)th);
+        }
+        if (active) {
+          bad |= !(finite4(lv[k]) && finite4(vk));
+          *reinterpret_cast<float4*>(a.L + k * a.N + e0) = lv[k];
+          *reinterpret_cast<float4*>(a.M + k * a.N + e0) = mk;
+          if (!lion) *reinterpret_cast<float4*>(a.V + k * a.N + e0) = vk;
+        }
       }
-    if (active) {
+    } else {
+      float4 mv[K], vv[K];
 #pragma unroll
       for (int k = 0; k < K; ++k) {
-        bad |= !(__builtin_isfinite(lv[k].x) && __builtin_isfinite(lv[k].y) &&
-                 __builtin_isfinite(lv[k].z) && __builtin_isfinite(lv[k].w) &&
-                 __builtin_isfinite(vv[k].x) && __builtin_isfinite(vv[k].y) &&
-                 __builtin_isfinite(vv[k].z) && __builtin_isfinite(vv[k].w));
-        *reinterpret_cast<float4*>(a.L + k * a.N + e0) = lv[k];
-        *reinterpret_cast<float4*>(a.M + k * a.N + e0) = mv[k];
-        if (!lion) *reinterpret_cast<float4*>(a.V + k * a.N + e0) = vv[k];
+        mv[k] = active ? *reinterpret_cast<const float4*>(a.M + k * a.N + e0)
+                       : make_float4(0.f, 0.f, 0.f, 0.f);
+        vv[k] = (active && !lion) ? *reinterpret_cast<const float4*>(a.V + k * a.N + e0)
+                                  : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          T th = (T)f4get(lv[k], q), m1 = (T)f4get(mv[k], q), v1 = (T)f4get(vv[k], q);
+          opt_update<kF64>(lion, dacc[q][k], th, m1, v1, lr, step_l, b1, b2, omb1, omb2, rbc2,
+                           eps, wd);
+          f4set(mv[k], q, (float)m1);
+          f4set(vv[k], q, (float)v1);
+          f4set(lv[k], q, (float)th);
+        }
+      if (active) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          bad |= !(finite4(lv[k]) && finite4(vv[k]));
+          *reinterpret_cast<float4*>(a.L + k * a.N + e0) = lv[k];
+          *reinterpret_cast<float4*>(a.M + k * a.N + e0) = mv[k];
+          if (!lion) *reinterpret_cast<float4*>(a.V + k * a.N + e0) = vv[k];
+        }
       }
     }
     float s_new = s32;
