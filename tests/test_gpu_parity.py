@@ -22,6 +22,12 @@ pytestmark = pytest.mark.gpu
 
 TOL = {"fp32": 1e-5, "bf16": 1e-3}
 L3, L4, L8 = inputs.L3, inputs.L4, inputs.L8
+# other symmetric grids: 2, 5, 6 and 7 levels (the backward updates the moments plane by plane
+# for 5 to 7)
+L2 = (-0.5, 0.5)
+L5 = (-2.0, -1.0, 0.0, 1.0, 2.0)
+L6 = (-2.5, -1.5, -0.5, 0.5, 1.5, 2.5)
+L7 = (-3.0, -2.0, -1.0, 0.0, 1.0, 2.0, 3.0)
 
 
 @pytest.fixture(scope="module")
@@ -104,13 +110,19 @@ CASES = [
     ("bf16", 3, 40, 512, 8, 16, "superblock", 0.3, 1.0),
     ("fp32", 1, 1, 16, 3, 16, "group", 0.5, 1.0),       # one row, 16 columns: almost all padding
     ("bf16", 5, 7, 48, 4, 16, "group", 0.3, 1.0),       # five small layers, ragged everywhere
+    ("bf16", 1, 66, 256, 2, 32, "group", 0.4, 1.0),
+    ("bf16", 1, 66, 512, 5, 128, "group", 0.2, 1.0),
+    ("bf16", 2, 33, 256, 6, 64, "group", 0.5, 1.0),
+    ("bf16", 1, 40, 384, 7, 128, "group", 0.1, 1.0),
+    ("fp32", 1, 24, 256, 6, 64, "group", 0.3, 1.0),
+    ("fp32", 1, 24, 256, 8, 128, "group", 0.3, 1.0),
 ]
 
 
 @pytest.mark.parametrize("prec,batch,O,I,K,gs,layout,tau,kappa", CASES)
 @pytest.mark.parametrize("warm", [False, True])
 def test_single_step_matches_oracle(dev, prec, batch, O, I, K, gs, layout, tau, kappa, warm):
-    levels = {3: L3, 4: L4, 8: L8}[K]
+    levels = {2: L2, 3: L3, 4: L4, 5: L5, 6: L6, 7: L7, 8: L8}[K]
     W, H = layer_inputs(O, I, batch=batch, bf16=prec == "bf16", seed=O + I)
     rcfg = ref.Config(O, I, levels, gs, batch=batch, layout=layout, precision=prec, seed=4)
     pair = Pair(rcfg, W, H, dev)
@@ -144,9 +156,10 @@ def test_single_step_matches_oracle(dev, prec, batch, O, I, K, gs, layout, tau, 
 
 # ------------------------------------------------------------------ harden / pack
 @pytest.mark.parametrize("K,gs,layout", [(4, 128, "group"), (3, 64, "group"), (8, 128, "group"),
-                                         (2, 16, "group"), (8, 16, "superblock")])
+                                         (2, 16, "group"), (5, 64, "group"), (7, 32, "group"),
+                                         (8, 16, "superblock")])
 def test_harden_and_pack_are_bit_exact(dev, K, gs, layout):
-    levels = {2: (-0.5, 0.5), 3: L3, 4: L4, 8: L8}[K]
+    levels = {2: L2, 3: L3, 4: L4, 5: L5, 7: L7, 8: L8}[K]
     O, I, batch = 37, 512, 2
     W, H = layer_inputs(O, I, batch=batch, seed=K)
     rcfg = ref.Config(O, I, levels, gs, batch=batch, layout=layout, precision="bf16", seed=2)
@@ -355,9 +368,10 @@ def test_full_size_layer_on_sampled_rows(dev, name):
 @pytest.mark.parametrize("opt", ["lion", "adamw"])
 @pytest.mark.parametrize("prec,O,I,K,gs,tau", [("fp32", 256, 256, 4, 128, 0.2),
                                                ("bf16", 200, 384, 3, 128, 0.5),
-                                               ("bf16", 130, 512, 8, 64, 0.1)])
+                                               ("bf16", 130, 512, 8, 64, 0.1),
+                                               ("bf16", 66, 512, 6, 64, 0.3)])
 def test_lion_and_adamw_single_step(dev, opt, prec, O, I, K, gs, tau):
-    levels = {3: L3, 4: L4, 8: L8}[K]
+    levels = {3: L3, 4: L4, 6: L6, 8: L8}[K]
     W, H = layer_inputs(O, I, bf16=prec == "bf16", seed=O + 3 * I)
     rcfg = ref.Config(O, I, levels, gs, precision=prec, seed=6)
     pair = Pair(rcfg, W, H, dev)
@@ -407,10 +421,11 @@ def test_lion_tiny_layer_trajectory(dev):
     ("fp32", 70, 384, 3, 64, 3),
     ("bf16", 200, 384, 3, 128, 4),
     ("bf16", 130, 512, 8, 128, 2),
+    ("bf16", 66, 512, 7, 128, 3),
 ])
 def test_multi_sample_step(dev, prec, O, I, K, gs, M):
     """M independent Gumbel draws in one step, gradients and loss averaged (§3.3)."""
-    levels = {3: L3, 4: L4, 8: L8}[K]
+    levels = {3: L3, 4: L4, 7: L7, 8: L8}[K]
     W, H = layer_inputs(O, I, bf16=prec == "bf16", seed=O + 5 * I)
     rcfg = ref.Config(O, I, levels, gs, precision=prec, seed=8)
     pair = Pair(rcfg, W, H, dev)
