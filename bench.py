@@ -99,11 +99,21 @@ def cpu_baseline(w, W, H, rows, steps, lr_scales, opt_kw):
     """The oracle, untuned, on ``rows`` rows of the layer for ``steps`` steps (host cores)."""
     import numpy as np
     from oracle import gsq as ref
+    blas = []
     try:
         from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+        info = threadpool_info()
+        threads = max([p.get("num_threads", 1) for p in info] or [1])
+        blas = [f"{p.get('internal_api')} {p.get('version')} ({p.get('num_threads')} threads)"
+                for p in info if p.get("user_api") == "blas"]
     except Exception:
         threads = os.cpu_count()
+    cpu_model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), None)
+    except OSError:
+        pass
     rcfg = ref.Config(w.out_features, w.in_features, w.levels, w.group_size, batch=w.batch,
                       layout=w.layout, precision=w.precision, seed=0, relaxation=w.relaxation,
                       alpha=3.0 if w.relaxation == "ternary" else 6.0)
@@ -119,7 +129,8 @@ def cpu_baseline(w, W, H, rows, steps, lr_scales, opt_kw):
     return {"value": frac / sec, "unit": "steps/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{len(sel)} of {w.out_features} rows x {steps} steps "
                       f"({sec:.2f} s/step), scaled to the whole layer by the row fraction",
-            "cpu_count": os.cpu_count()}
+            "cpu_count": os.cpu_count(), "cpu_model": cpu_model, "numpy": np.__version__,
+            "blas": blas}
 
 
 def copy_calibration(dev, gib=1):
