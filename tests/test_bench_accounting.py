@@ -61,3 +61,22 @@ def test_harden_bytes():
     n = w.out_features * w.in_features
     assert b.harden_bytes(w, hard_loss=False) == n * (12 + 1) + n // 128 * 8
     assert b.harden_bytes(w, hard_loss=True) == n * (12 + 1 + 4) + n // 128 * 8
+
+
+def test_recorded_backward_traffic_matches_the_algorithmic_bytes():
+    """The HBM bytes measured for the backward (FETCH_SIZE + WRITE_SIZE, copy-calibrated) stay
+    within a few percent of what the step must move: the kernel re-reads nothing."""
+    import json
+    b = _bench()
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    rec = json.load(open(path))
+    checked = 0
+    for key, r in rec.items():
+        kernel, name = key.split(":", 1)
+        if kernel != "backward" or name not in inputs.WORKLOADS:
+            continue
+        w = inputs.WORKLOADS[name]
+        alg = b.algorithmic_work(w, fused=True, want_loss=True, lr_scales=w.lr_scales)["backward"][1]
+        assert 0.98 <= r["bytes_per_launch"] / alg <= 1.05, (name, r["bytes_per_launch"], alg)
+        checked += 1
+    assert checked >= 2
