@@ -236,7 +236,8 @@ gsq_status gsq_layer_init(const gsq_config* cfg, const void* W, int32_t w_dtype,
   }
   bool ok = alloc(&L.W, L.N * (L.w_bf16 ? 2 : 4)) &&
             alloc(&L.H, (size_t)(L.B * L.Ipad * L.Ipad) * relem) &&
-            alloc(&L.L, L.K * L.N * 4) && alloc(&L.M, L.K * L.N * 4) && alloc(&L.V, L.K * L.N * 4) &&
+            alloc(&L.L, gsq::state_floats(L) * 4) && alloc(&L.M, gsq::state_floats(L) * 4) &&
+            alloc(&L.V, gsq::state_floats(L) * 4) &&
             alloc(&L.S, L.NG * 4) && alloc(&L.MS, L.NG * 4) && alloc(&L.VS, L.NG * 4) &&
             alloc(&L.R[0], npad * relem) && alloc(&L.R[1], npad * relem) &&
             alloc(&L.G, npad * 4) && alloc(&L.partials, (size_t)(L.B * L.tiles_per_batch) * 8) &&
@@ -258,8 +259,8 @@ gsq_status gsq_layer_init(const gsq_config* cfg, const void* W, int32_t w_dtype,
     GSQ_HIP(timed(L, GSQ_KERNEL_INIT, stream, [&] { return gsq::launch_symmetrize_h(H, L.H, L.B, L.I, L.Ipad, L.bf16, stream); }));
     GSQ_HIP(hipMemsetAsync(L.R[0], 0, npad * relem, stream));   // padding stays zero
     GSQ_HIP(hipMemsetAsync(L.R[1], 0, npad * relem, stream));
-    GSQ_HIP(hipMemsetAsync(L.M, 0, L.K * L.N * 4, stream));
-    GSQ_HIP(hipMemsetAsync(L.V, 0, L.K * L.N * 4, stream));
+    GSQ_HIP(hipMemsetAsync(L.M, 0, gsq::state_floats(L) * 4, stream));
+    GSQ_HIP(hipMemsetAsync(L.V, 0, gsq::state_floats(L) * 4, stream));
     GSQ_HIP(hipMemsetAsync(L.MS, 0, L.NG * 4, stream));
     GSQ_HIP(hipMemsetAsync(L.VS, 0, L.NG * 4, stream));
     GSQ_HIP(hipMemsetAsync(L.flag, 0, sizeof(int), stream));

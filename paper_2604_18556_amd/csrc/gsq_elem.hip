@@ -37,6 +37,13 @@ __device__ __forceinline__ bool finite4(const float4& v) {
          __builtin_isfinite(v.w);
 }
 
+// Float offset of logit (or moment) k of coordinate e in the blocked state layout.  Four
+// consecutive coordinates from a multiple of 4 lie in one block, so a lane's float4 is
+// contiguous and 16-byte aligned.
+__device__ __forceinline__ int64_t state_off(int64_t e, int k, int K) {
+  return (e / kStateBlock) * (K * kStateBlock) + (int64_t)k * kStateBlock + (e % kStateBlock);
+}
+
 __device__ __forceinline__ void load_w4(const void* W, int w_bf16, int64_t e, float (&w)[4]) {
   if (w_bf16) {
     const uint2 u = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(W) + e);
@@ -248,7 +255,7 @@ __global__ __launch_bounds__(kBlock) void k_forward(ElemArgs a) {
     load_w4(a.W, a.w_bf16, e0, w);
     float4 lv[K];
 #pragma unroll
-    for (int k = 0; k < K; ++k) lv[k] = *reinterpret_cast<const float4*>(a.L + k * a.N + e0);
+    for (int k = 0; k < K; ++k) lv[k] = *reinterpret_cast<const float4*>(a.L + state_off(e0, k, K));
     const uint32_t j4 = chunk_bases<kMode>(a, e0);
     float g[4][Z];
     chunk_noise<Z, kF64>(g, a, (uint64_t)e0, a.t, (uint32_t)a.sample);
@@ -376,7 +383,7 @@ __global__ __launch_bounds__(kBlock, (backward_min_blocks<K, kF64, kScales, kMul
     const int64_t gidx = active ? padded_index(a, row, col0) : 0;
 #pragma unroll
     for (int k = 0; k < K; ++k)
-      lv[k] = active ? *reinterpret_cast<const float4*>(a.L + k * a.N + e0)
+      lv[k] = active ? *reinterpret_cast<const float4*>(a.L + state_off(e0, k, K))
                      : make_float4(0.f, 0.f, 0.f, 0.f);
     const uint32_t j4 = chunk_bases<kMode>(a, e0);
     float w[4] = {0.f, 0.f, 0.f, 0.f};
@@ -433,9 +440,9 @@ __global__ __launch_bounds__(kBlock, (backward_min_blocks<K, kF64, kScales, kMul
     if constexpr (backward_plane_update<K, kScales, kMode>()) {
 #pragma unroll
       for (int k = 0; k < K; ++k) {
-        float4 mk = active ? *reinterpret_cast<const float4*>(a.M + k * a.N + e0)
+        float4 mk = active ? *reinterpret_cast<const float4*>(a.M + state_off(e0, k, K))
                            : make_float4(0.f, 0.f, 0.f, 0.f);
-        float4 vk = (active && !lion) ? *reinterpret_cast<const float4*>(a.V + k * a.N + e0)
+        float4 vk = (active && !lion) ? *reinterpret_cast<const float4*>(a.V + state_off(e0, k, K))
                                       : make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -448,18 +455,19 @@ __global__ __launch_bounds__(kBlock, (backward_min_blocks<K, kF64, kScales, kMul
         }
         if (active) {
           bad |= !(finite4(lv[k]) && finite4(vk));
-          *reinterpret_cast<float4*>(a.L + k * a.N + e0) = lv[k];
-          *reinterpret_cast<float4*>(a.M + k * a.N + e0) = mk;
-          if (!lion) *reinterpret_cast<float4*>(a.V + k * a.N + e0) = vk;
+          const int64_t o = state_off(e0, k, K);
+          *reinterpret_cast<float4*>(a.L + o) = lv[k];
+          *reinterpret_cast<float4*>(a.M + o) = mk;
+          if (!lion) *reinterpret_cast<float4*>(a.V + o) = vk;
         }
       }
     } else {
       float4 mv[K], vv[K];
 #pragma unroll
       for (int k = 0; k < K; ++k) {
-        mv[k] = active ? *reinterpret_cast<const float4*>(a.M + k * a.N + e0)
+        mv[k] = active ? *reinterpret_cast<const float4*>(a.M + state_off(e0, k, K))
                        : make_float4(0.f, 0.f, 0.f, 0.f);
-        vv[k] = (active && !lion) ? *reinterpret_cast<const float4*>(a.V + k * a.N + e0)
+        vv[k] = (active && !lion) ? *reinterpret_cast<const float4*>(a.V + state_off(e0, k, K))
                                   : make_float4(0.f, 0.f, 0.f, 0.f);
       }
 #pragma unroll
@@ -477,9 +485,10 @@ __global__ __launch_bounds__(kBlock, (backward_min_blocks<K, kF64, kScales, kMul
 #pragma unroll
         for (int k = 0; k < K; ++k) {
           bad |= !(finite4(lv[k]) && finite4(vv[k]));
-          *reinterpret_cast<float4*>(a.L + k * a.N + e0) = lv[k];
-          *reinterpret_cast<float4*>(a.M + k * a.N + e0) = mv[k];
-          if (!lion) *reinterpret_cast<float4*>(a.V + k * a.N + e0) = vv[k];
+          const int64_t o = state_off(e0, k, K);
+          *reinterpret_cast<float4*>(a.L + o) = lv[k];
+          *reinterpret_cast<float4*>(a.M + o) = mv[k];
+          if (!lion) *reinterpret_cast<float4*>(a.V + o) = vv[k];
         }
       }
     }
@@ -644,7 +653,8 @@ __global__ void k_init_logits(const void* W, int w_bf16, const float* S, float* 
       }
     }
     for (int k = 0; k < ic.K; ++k)
-      L[k * N + e] = (float)((double)ic.sigma * ((double)eps[k] + (double)ic.alpha * (mu[k] - mean)));
+      L[state_off(e, k, ic.K)] =
+          (float)((double)ic.sigma * ((double)eps[k] + (double)ic.alpha * (mu[k] - mean)));
   }
 }
 
@@ -667,15 +677,15 @@ __global__ __launch_bounds__(kBlock) void k_harden(ElemArgs a, int K, int relax,
     const int64_t e0 = row * a.I + col0;
     int q[4] = {0, 0, 0, 0};
     if (relax == GSQ_RELAX_TERNARY) {
-      const float4 mask = *reinterpret_cast<const float4*>(a.L + e0);
-      const float4 sign = *reinterpret_cast<const float4*>(a.L + a.N + e0);
+      const float4 mask = *reinterpret_cast<const float4*>(a.L + state_off(e0, 0, 2));
+      const float4 sign = *reinterpret_cast<const float4*>(a.L + state_off(e0, 1, 2));
 #pragma unroll
       for (int j = 0; j < 4; ++j)
         q[j] = f4get(mask, j) >= 0.f ? (f4get(sign, j) >= 0.f ? 2 : 0) : 1;
     } else {
-      float4 best = *reinterpret_cast<const float4*>(a.L + e0);
+      float4 best = *reinterpret_cast<const float4*>(a.L + state_off(e0, 0, K));
       for (int k = 1; k < K; ++k) {
-        const float4 x = *reinterpret_cast<const float4*>(a.L + k * a.N + e0);
+        const float4 x = *reinterpret_cast<const float4*>(a.L + state_off(e0, k, K));
         if (x.x > best.x) { best.x = x.x; q[0] = k; }
         if (x.y > best.y) { best.y = x.y; q[1] = k; }
         if (x.z > best.z) { best.z = x.z; q[2] = k; }
@@ -795,13 +805,13 @@ __global__ void k_pack_superblock(const uint8_t* codes, const uint16_t* D, const
 }
 
 // ------------------------------------------------------------------ state copies
-// Between the caller's coordinate-major layout (B, O, I, K) and the K planes.
+// Between the caller's coordinate-major layout (B, O, I, K) and the blocked planes.
 __global__ void k_state_io(float* inter, float* planar, int64_t N, int K, int to_planar) {
   for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < N;
        e += (int64_t)gridDim.x * blockDim.x) {
     for (int k = 0; k < K; ++k) {
-      if (to_planar) planar[k * N + e] = inter[e * K + k];
-      else inter[e * K + k] = planar[k * N + e];
+      if (to_planar) planar[state_off(e, k, K)] = inter[e * K + k];
+      else inter[e * K + k] = planar[state_off(e, k, K)];
     }
   }
 }
@@ -845,6 +855,10 @@ dim3 row_grid(const Layer& L) {
 }
 
 }  // namespace
+
+int64_t state_floats(const Layer& L) {
+  return L.K * ((L.N + kStateBlock - 1) / kStateBlock) * kStateBlock;
+}
 
 // ====================================================================== launchers
 ElemArgs base_args(const Layer& L) {

@@ -13,6 +13,10 @@ namespace gsq {
 constexpr int kTileM = 256;   // contraction tile (rows of R / G)
 constexpr int kTileN = 256;   // contraction tile (columns of G = rows of H)
 constexpr int kPadK = 256;    // padding of the inner dimension (H is padded with zeros)
+// Layout of the logits and of each optimiser moment: blocks of kStateBlock consecutive
+// coordinates, the K planes of a block side by side (plane k of block j starts at float
+// (j K + k) kStateBlock).  The arrays hold whole blocks.
+constexpr int64_t kStateBlock = 16384;
 
 // Everything an elementwise kernel needs, passed by value.
 struct ElemArgs {
@@ -49,6 +53,9 @@ struct ElemArgs {
   float kappa_n, inv_tau_n;
   double inv_tau_n_d;
 };
+
+struct Layer;
+int64_t state_floats(const Layer& L);   // floats of one logit / moment array
 
 struct Layer {
   gsq_config cfg;
