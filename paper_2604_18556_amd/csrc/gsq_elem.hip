@@ -2,11 +2,12 @@
 // the Gumbel-Softmax sample of Alg. 1 and its residual, the fused gradient + Adam pass,
 // hardening (argmax of Alg. 2) and bit-packing.
 //
-// Data layout in HBM: logits and both Adam moments are K planes of N = B*O*I fp32 values
-// (plane k holds level k of every coordinate, row-major), so every plane streams with
-// 16-byte loads across a wavefront.  A wavefront owns 256 consecutive columns of one row;
-// lane l owns columns 4l..4l+3.  Scale groups (16..256 columns) therefore lie inside one
-// wavefront and their gradient is reduced with lane shuffles in a fixed order.
+// Data layout in HBM: logits and both optimiser moments are K planes of fp32 values, laid out
+// in blocks of kStateBlock coordinates (row-major over B*O*I) with the K planes of a block side
+// by side, so every plane streams with 16-byte loads across a wavefront and a wavefront's planes
+// lie close together in memory.  A wavefront owns 256 consecutive columns of one row; lane l
+// owns columns 4l..4l+3.  Scale groups (16..256 columns) therefore lie inside one wavefront and
+// their gradient is reduced with lane shuffles in a fixed order.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 

@@ -23,7 +23,7 @@ struct ElemArgs {
   const void* W;        // B*O*I, fp32 or bf16
   const float* G;       // B*Opad*Ipad fp32
   void* Rout;           // B*Opad*Ipad, fp32 (FP32 path) or bf16
-  float *L, *M, *V;     // K planes of N fp32 each (K = logits per coordinate)
+  float *L, *M, *V;     // K planes each, in blocks of kStateBlock coordinates (K = logits per coordinate)
   const uint8_t* J0;    // local shift: initial grid index of every coordinate (N bytes)
   float *S, *MS, *VS;   // one per scale group
   int* flag;            // sticky non-finite flag
