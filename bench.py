@@ -133,6 +133,34 @@ def cpu_baseline(w, W, H, rows, steps, lr_scales, opt_kw):
             "blas": blas}
 
 
+def library_gemm(w, dev, reps=20):
+    """The same contraction through the vendor BLAS (torch.mm: bf16 operands, fp32 output, as G
+    needs), for one layer of the workload, as a reference beside the library's own kernel."""
+    import torch
+    O, I = w.out_features, w.in_features
+    gen = torch.Generator(device=dev).manual_seed(0)
+    a = torch.randn(O, I, device=dev, dtype=torch.bfloat16, generator=gen)
+    b = torch.randn(I, I, device=dev, dtype=torch.bfloat16, generator=gen)
+
+    def f():
+        return torch.mm(a, b.t(), out_dtype=torch.float32)
+    for _ in range(3):
+        f()
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(reps):
+        f()
+    e.record()
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / reps
+    del a, b
+    return {"ms_per_layer": ms, "ms_per_step": ms * w.batch,
+            "TFLOP/s": 2.0 * O * I * I / (ms * 1e-3) / 1e12,
+            "note": "torch.mm of a bf16 O x I by a bf16 I x I matrix with fp32 output "
+                    "(hipBLASLt), not part of the step"}
+
+
 def copy_calibration(dev, gib=1):
     import torch
     n = gib * (1 << 30) // 4
@@ -158,6 +186,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--loss-every", type=int, default=1, help="request the loss every n steps")
+    ap.add_argument("--no-library-gemm", action="store_true",
+                    help="skip timing the same contraction through the vendor BLAS")
     ap.add_argument("--no-fuse", action="store_true", help="do not draw the next sample in the backward pass")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=512)
@@ -289,6 +319,13 @@ def main():
     h_bytes = harden_bytes(w, hard_loss=True)
     p_ms = once_pack["pack"][0]
 
+    lib_gemm = None
+    if w.precision == "bf16" and not args.no_library_gemm:
+        try:
+            lib_gemm = library_gemm(w, dev)
+        except (RuntimeError, TypeError) as ex:   # an older torch without out_dtype
+            lib_gemm = {"error": str(ex)[:200]}
+
     cpu = None
     if not args.no_cpu_baseline:
         ref_opt = dict(samples=args.samples)
@@ -332,6 +369,7 @@ def main():
                            "note": "harden: codes, hard residual and fp16 scales (gsq_harden with "
                                    "a hard loss); pack: the bit-packing kernels of gsq_pack, which "
                                    "first re-derives the codes (pack_harden_ms)"},
+        "library_gemm": lib_gemm,
         "gpu_vs_cpu": None if cpu is None else (1e3 / ms_step) / cpu["value"],
     }
     print(json.dumps(out), flush=True)
