@@ -298,7 +298,8 @@ FULL_SIZE = ["attn-4096x4096-k3", "attn-4096x4096-ternary", "mlp-up-14336x4096-k
 def test_full_size_layer_on_sampled_rows(dev, name):
     """A full-size workload in the benchmark's launch configuration (next sample drawn by the
     backward pass, loss every step): init and two steps, sampled rows (first, second, interior,
-    middle, last) of sampled experts vs the oracle."""
+    middle, last) of sampled experts vs the oracle; after the first step, the whole contraction
+    of those experts (every element of G) vs the vendor BLAS."""
     w = inputs.WORKLOADS[name]
     W, Hd = inputs.make_layer(w, device=dev)
     experts = [0] if w.batch == 1 else [0, 37, w.batch - 1]
@@ -314,6 +315,9 @@ def test_full_size_layer_on_sampled_rows(dev, name):
                              relaxation={"shift": B.RELAX_SHIFT, "ternary": B.RELAX_TERNARY}.get(
                                  w.relaxation, B.RELAX_GRID))
     layer = B.Layer(pair_cfg, torch.from_numpy(W).to(dev).to(torch.bfloat16), Hd)
+    # the library's bf16 H of the sampled experts, (H + H^T) / 2 rounded to nearest even: exactly
+    # symmetric, so it serves as the right operand without a transposed view
+    Hs_bf = {e: ((Hd[e] + Hd[e].t()) * 0.5).to(torch.bfloat16) for e in experts}
     torch.cuda.synchronize()
     del Hd                                   # the library keeps its own copy of H
     torch.cuda.empty_cache()
@@ -346,6 +350,17 @@ def test_full_size_layer_on_sampled_rows(dev, name):
         G = torch.empty(Bn, O, I, device=dev)
         layer.intermediates(grad=G)
         G_rows = G[experts][:, rows].cpu().numpy()
+        if t == 0:
+            # the whole contraction of the sampled experts against the vendor BLAS (independent
+            # code, fp32 accumulation in another order): G = -2 R H in every element
+            R = torch.empty(Bn, O, I, dtype=torch.bfloat16, device=dev)
+            layer.intermediates(residual=R)
+            for e in experts:
+                P = torch.mm(R[e], Hs_bf[e], out_dtype=torch.float32)
+                err = ((G[e] + 2.0 * P).abs().max() / (2.0 * P).abs().max()).item()
+                assert err <= 1e-4, (name, e, err)
+                del P
+            del R
         del G
         st_new, _, inter = ref.step(rcfg, W, Hs, st, oracle_params(prm), rows=rows, want=True,
                                     batches=experts)
