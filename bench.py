@@ -200,8 +200,8 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU: the GSQ layer step is measured per GPU and this build has "
-              f"no multi-GPU path (asked for --gpus {args.gpus})", file=sys.stderr)
+        print(f"bench.py runs on one GPU: the GSQ layer step is measured per GPU and the library "
+              f"has no multi-GPU path (asked for --gpus {args.gpus})", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
