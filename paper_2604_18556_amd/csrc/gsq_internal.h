@@ -120,7 +120,7 @@ ElemArgs base_args(const Layer& L);
 
 // ---- launchers (gsq_contract.hip)
 int64_t contract_tiles_per_batch(const Layer& L);
-// Let the BF16 contraction use its 128 KB of LDS on the current device (called at init).
+// Let the BF16 contraction use its 160 KB of LDS on the current device (called at init).
 hipError_t prepare_contract_kernel();
 int64_t loss_stage_size(const Layer& L);   // doubles
 // Split the K range of the tiles of a last, at most half-full round of the GPU's num_cu
