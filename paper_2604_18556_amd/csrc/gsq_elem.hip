@@ -666,8 +666,9 @@ __global__ void k_init_logits(const void* W, int w_bf16, const float* S, float* 
 // fp16 in the group layouts) written in the contraction's padded layout, fp32 when
 // r_f32 != 0, bf16 otherwise.  Rows and columns as in the forward: four rows per block, four
 // consecutive columns per lane (I is a multiple of 16, so a lane's columns share a group).
-__global__ __launch_bounds__(kBlock) void k_harden(ElemArgs a, int K, int relax, int superblock,
-                                                   int r_f32, uint8_t* codes, void* Rh) {
+template <int K, int kMode>
+__global__ __launch_bounds__(kBlock) void k_harden(ElemArgs a, int superblock, int r_f32,
+                                                   uint8_t* codes, void* Rh) {
   const int lane = threadIdx.x & 63;
   const int64_t col0 = (int64_t)blockIdx.x * kCols + lane * 4;
   const int64_t gpr = a.I / a.gs;
@@ -676,23 +677,33 @@ __global__ __launch_bounds__(kBlock) void k_harden(ElemArgs a, int K, int relax,
        row += (int64_t)gridDim.y * 4) {
     if (col0 >= a.I) continue;
     const int64_t e0 = row * a.I + col0;
+    // every load (logit planes, and W and the scale for the hard residual) is issued before the
+    // first comparison and before the byte store of the codes, which the compiler may not move
+    // loads across
+    float4 lv[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) lv[k] = *reinterpret_cast<const float4*>(a.L + state_off(e0, k, K));
+    float w[4] = {0.f, 0.f, 0.f, 0.f}, s = 0.f;
+    if (Rh) {
+      s = a.S[row * gpr + col0 / a.gs];
+      load_w4(a.W, a.w_bf16, e0, w);
+    }
     int q[4] = {0, 0, 0, 0};
-    if (relax == GSQ_RELAX_TERNARY) {
-      const float4 mask = *reinterpret_cast<const float4*>(a.L + state_off(e0, 0, 2));
-      const float4 sign = *reinterpret_cast<const float4*>(a.L + state_off(e0, 1, 2));
+    if constexpr (kMode == GSQ_RELAX_TERNARY) {
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        q[j] = f4get(mask, j) >= 0.f ? (f4get(sign, j) >= 0.f ? 2 : 0) : 1;
+        q[j] = f4get(lv[0], j) >= 0.f ? (f4get(lv[1], j) >= 0.f ? 2 : 0) : 1;
     } else {
-      float4 best = *reinterpret_cast<const float4*>(a.L + state_off(e0, 0, K));
+      float4 best = lv[0];
+#pragma unroll
       for (int k = 1; k < K; ++k) {
-        const float4 x = *reinterpret_cast<const float4*>(a.L + state_off(e0, k, K));
+        const float4 x = lv[k];
         if (x.x > best.x) { best.x = x.x; q[0] = k; }
         if (x.y > best.y) { best.y = x.y; q[1] = k; }
         if (x.z > best.z) { best.z = x.z; q[2] = k; }
         if (x.w > best.w) { best.w = x.w; q[3] = k; }
       }
-      if (relax == GSQ_RELAX_SHIFT) {
+      if constexpr (kMode == GSQ_RELAX_SHIFT) {
         const uint32_t j4 = *reinterpret_cast<const uint32_t*>(a.J0 + e0);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -713,10 +724,8 @@ __global__ __launch_bounds__(kBlock) void k_harden(ElemArgs a, int K, int relax,
       }
     }
     if (Rh) {
-      float s = a.S[row * gpr + col0 / a.gs];
       if (!superblock) s = __half2float(__float2half_rn(s));
-      float w[4], r[4];
-      load_w4(a.W, a.w_bf16, e0, w);
+      float r[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         float cq = a.c[0];
@@ -977,11 +986,25 @@ hipError_t launch_backward(const Layer& L, const ElemArgs& a, bool update_scales
   }
 }
 
-hipError_t launch_harden(const Layer& L, uint8_t* codes, void* Rh, hipStream_t s) {
-  const ElemArgs a = base_args(L);
-  hipLaunchKernelGGL(k_harden, row_grid(L), dim3(kBlock), 0, s, a, (int)L.K, L.relax,
+template <int K, int kMode = GSQ_RELAX_GRID>
+static hipError_t harden_k(const Layer& L, uint8_t* codes, void* Rh, hipStream_t s) {
+  hipLaunchKernelGGL((k_harden<K, kMode>), row_grid(L), dim3(kBlock), 0, s, base_args(L),
                      L.cfg.layout == GSQ_LAYOUT_SUPERBLOCK ? 1 : 0, L.bf16 ? 0 : 1, codes, Rh);
   return hipGetLastError();
+}
+
+hipError_t launch_harden(const Layer& L, uint8_t* codes, void* Rh, hipStream_t s) {
+  if (L.relax == GSQ_RELAX_SHIFT) return harden_k<GSQ_SHIFT_WINDOW, GSQ_RELAX_SHIFT>(L, codes, Rh, s);
+  if (L.relax == GSQ_RELAX_TERNARY) return harden_k<2, GSQ_RELAX_TERNARY>(L, codes, Rh, s);
+  switch (L.K) {
+    case 2: return harden_k<2>(L, codes, Rh, s);
+    case 3: return harden_k<3>(L, codes, Rh, s);
+    case 4: return harden_k<4>(L, codes, Rh, s);
+    case 5: return harden_k<5>(L, codes, Rh, s);
+    case 6: return harden_k<6>(L, codes, Rh, s);
+    case 7: return harden_k<7>(L, codes, Rh, s);
+    default: return harden_k<8>(L, codes, Rh, s);
+  }
 }
 
 hipError_t launch_eff_scales(const Layer& L, float* out, hipStream_t s) {
