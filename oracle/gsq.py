@@ -368,13 +368,15 @@ def forward(cfg, W, logits, s_coord, g, tau, kappa, cand=None):
     return p, v, to_contraction_precision(cfg, R)
 
 
-def contract(cfg, R, Hs):
+def contract(cfg, R, Hs, Hc=None):
     """P = R H and the loss L = sum(R * P) = tr(R H R^T) (Eq. 1 for a linear layer).
 
     ``Hs`` is the symmetrised float32 H; in the bf16 precision it is rounded to
-    bfloat16 first.  Accumulation is float64.
+    bfloat16 first.  Accumulation is float64.  ``Hc``, when given, is that rounded
+    operand computed beforehand (long runs round H once; the values are the same).
     """
-    Hc = to_contraction_precision(cfg, Hs)
+    if Hc is None:
+        Hc = to_contraction_precision(cfg, Hs)
     P = R @ Hc
     return P, float((R * P).sum())
 
@@ -488,7 +490,7 @@ def update(prm, theta, m, v, grad, lr, n):
     return adam(theta, m, v, grad, lr, prm.beta1, prm.beta2, prm.eps, n, prm.weight_decay)
 
 
-def step(cfg, W, Hs, st, prm, rows=None, want=False, batches=None):
+def step(cfg, W, Hs, st, prm, rows=None, want=False, batches=None, Hc=None):
     """One GSQ optimisation step on state ``st`` (returns a new state, the loss).
 
     Order: noise -> soft sample -> residual -> contraction and loss -> gradient
@@ -503,7 +505,8 @@ def step(cfg, W, Hs, st, prm, rows=None, want=False, batches=None):
     then holds just those rows and layers, ``Hs`` just those layers' H, and noise
     indices stay the global ones.
     ``want`` returns the intermediates (g, p, v, R, G of the last sample; the averaged
-    dlogits, dscales).
+    dlogits, dscales).  ``Hc`` optionally holds ``to_contraction_precision(cfg, Hs)``
+    of the same layers, computed once for a run of many steps.
     """
     B, O, I, K = cfg.batch, cfg.out_features, cfg.in_features, cfg.K
     prm = as_f32_params(prm)
@@ -532,7 +535,7 @@ def step(cfg, W, Hs, st, prm, rows=None, want=False, batches=None):
                 p, v, R = ternary_forward(cfg, W[b], lg, s_coord, g, prm.tau, prm.kappa)
             else:
                 p, v, R = forward(cfg, W[b], lg, s_coord, g, prm.tau, prm.kappa, cand)
-            P, L = contract(cfg, R, Hs[b])
+            P, L = contract(cfg, R, Hs[b], None if Hc is None else Hc[b])
             G = -2.0 * P
             if cfg.relaxation == "ternary":
                 dl1, ds1 = ternary_backward(cfg, G[None], s_coord[None], p[None], prm.tau, prm.kappa)

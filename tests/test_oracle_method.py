@@ -79,6 +79,23 @@ def test_loss_through_H_equals_output_error_from_X():
     assert abs(L - direct) <= 1e-12 * direct
 
 
+def test_step_with_the_contraction_operand_rounded_beforehand_is_identical():
+    """Long runs pass H already rounded to the contraction's precision: same values, same step."""
+    rng = np.random.default_rng(4)
+    cfg = gsq.Config(8, 256, L4, 128, batch=2, precision="bf16", seed=3)
+    W = rng.normal(0, 0.02, (2, 8, 256))
+    Hs = gsq.symmetrize(np.stack([_spd(rng, 256)[1] for _ in range(2)]))
+    rows, batches = np.array([1, 6]), np.array([1])
+    st = gsq.init_layer(cfg, W, rows=rows, batches=batches)
+    prm = gsq.StepParams(tau=0.4, kappa=1.0, lr_logits=1e-2, lr_scales=5e-5)
+    a, la = gsq.step(cfg, W, Hs[batches], st, prm, rows=rows, batches=batches)
+    b, lb = gsq.step(cfg, W, Hs[batches], st, prm, rows=rows, batches=batches,
+                     Hc=gsq.to_contraction_precision(cfg, Hs[batches]))
+    np.testing.assert_array_equal(la, lb)
+    for k in ("logits", "m", "v", "scales", "m_s", "v_s"):
+        np.testing.assert_array_equal(getattr(a, k), getattr(b, k))
+
+
 def test_zero_loss_when_weights_lie_on_the_grid():
     """W = s c[q*] with each group reaching the outer level: init recovers s and q*, hard loss 0,
     and the noise-free optimisation keeps q* (it is the global optimum, loss 0)."""
