@@ -45,6 +45,26 @@ __device__ __forceinline__ int64_t state_off(int64_t e, int k, int K) {
   return (e / kStateBlock) * (K * kStateBlock) + (int64_t)k * kStateBlock + (e % kStateBlock);
 }
 
+// Streaming accesses of the state and G: each is touched once per launch, so the loads and
+// stores carry the non-temporal hint (no cache allocation).  On the backward's access pattern
+// this moves 14-21 % more bytes per second than plain accesses.  W and R keep plain accesses:
+// R is read next by the contraction, and the hint on them measured slightly slower.
+__device__ __forceinline__ float4 ld_stream(const float* p) {
+  float4 v;
+  v.x = __builtin_nontemporal_load(p);
+  v.y = __builtin_nontemporal_load(p + 1);
+  v.z = __builtin_nontemporal_load(p + 2);
+  v.w = __builtin_nontemporal_load(p + 3);
+  return v;
+}
+
+__device__ __forceinline__ void st_stream(float* p, const float4& v) {
+  __builtin_nontemporal_store(v.x, p);
+  __builtin_nontemporal_store(v.y, p + 1);
+  __builtin_nontemporal_store(v.z, p + 2);
+  __builtin_nontemporal_store(v.w, p + 3);
+}
+
 __device__ __forceinline__ void load_w4(const void* W, int w_bf16, int64_t e, float (&w)[4]) {
   if (w_bf16) {
     const uint2 u = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(W) + e);
@@ -384,7 +404,7 @@ __global__ __launch_bounds__(kBlock, (backward_min_blocks<K, kF64, kScales, kMul
     const int64_t gidx = active ? padded_index(a, row, col0) : 0;
 #pragma unroll
     for (int k = 0; k < K; ++k)
-      lv[k] = active ? *reinterpret_cast<const float4*>(a.L + state_off(e0, k, K))
+      lv[k] = active ? ld_stream(a.L + state_off(e0, k, K))
                      : make_float4(0.f, 0.f, 0.f, 0.f);
     const uint32_t j4 = chunk_bases<kMode>(a, e0);
     float w[4] = {0.f, 0.f, 0.f, 0.f};
@@ -399,7 +419,7 @@ __global__ __launch_bounds__(kBlock, (backward_min_blocks<K, kF64, kScales, kMul
       for (int k = 0; k < K; ++k) dacc[q][k] = 0;
     const int M = kMulti ? a.samples : 1;
     for (int smp = 0; smp < M; ++smp) {
-      const float4 gv = active ? *reinterpret_cast<const float4*>(a.G + smp * a.g_stride + gidx)
+      const float4 gv = active ? ld_stream(a.G + smp * a.g_stride + gidx)
                                : make_float4(0.f, 0.f, 0.f, 0.f);
       float g[4][Z];
       chunk_noise<Z, kF64>(g, a, (uint64_t)e0, a.t, (uint32_t)smp);
@@ -441,9 +461,9 @@ __global__ __launch_bounds__(kBlock, (backward_min_blocks<K, kF64, kScales, kMul
     if constexpr (backward_plane_update<K, kScales, kMode>()) {
 #pragma unroll
       for (int k = 0; k < K; ++k) {
-        float4 mk = active ? *reinterpret_cast<const float4*>(a.M + state_off(e0, k, K))
+        float4 mk = active ? ld_stream(a.M + state_off(e0, k, K))
                            : make_float4(0.f, 0.f, 0.f, 0.f);
-        float4 vk = (active && !lion) ? *reinterpret_cast<const float4*>(a.V + state_off(e0, k, K))
+        float4 vk = (active && !lion) ? ld_stream(a.V + state_off(e0, k, K))
                                       : make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -457,18 +477,18 @@ __global__ __launch_bounds__(kBlock, (backward_min_blocks<K, kF64, kScales, kMul
         if (active) {
           bad |= !(finite4(lv[k]) && finite4(vk));
           const int64_t o = state_off(e0, k, K);
-          *reinterpret_cast<float4*>(a.L + o) = lv[k];
-          *reinterpret_cast<float4*>(a.M + o) = mk;
-          if (!lion) *reinterpret_cast<float4*>(a.V + o) = vk;
+          st_stream(a.L + o, lv[k]);
+          st_stream(a.M + o, mk);
+          if (!lion) st_stream(a.V + o, vk);
         }
       }
     } else {
       float4 mv[K], vv[K];
 #pragma unroll
       for (int k = 0; k < K; ++k) {
-        mv[k] = active ? *reinterpret_cast<const float4*>(a.M + state_off(e0, k, K))
+        mv[k] = active ? ld_stream(a.M + state_off(e0, k, K))
                        : make_float4(0.f, 0.f, 0.f, 0.f);
-        vv[k] = (active && !lion) ? *reinterpret_cast<const float4*>(a.V + state_off(e0, k, K))
+        vv[k] = (active && !lion) ? ld_stream(a.V + state_off(e0, k, K))
                                   : make_float4(0.f, 0.f, 0.f, 0.f);
       }
 #pragma unroll
@@ -487,9 +507,9 @@ __global__ __launch_bounds__(kBlock, (backward_min_blocks<K, kF64, kScales, kMul
         for (int k = 0; k < K; ++k) {
           bad |= !(finite4(lv[k]) && finite4(vv[k]));
           const int64_t o = state_off(e0, k, K);
-          *reinterpret_cast<float4*>(a.L + o) = lv[k];
-          *reinterpret_cast<float4*>(a.M + o) = mv[k];
-          if (!lion) *reinterpret_cast<float4*>(a.V + o) = vv[k];
+          st_stream(a.L + o, lv[k]);
+          st_stream(a.M + o, mv[k]);
+          if (!lion) st_stream(a.V + o, vv[k]);
         }
       }
     }
@@ -682,7 +702,7 @@ __global__ __launch_bounds__(kBlock) void k_harden(ElemArgs a, int superblock, i
     // loads across
     float4 lv[K];
 #pragma unroll
-    for (int k = 0; k < K; ++k) lv[k] = *reinterpret_cast<const float4*>(a.L + state_off(e0, k, K));
+    for (int k = 0; k < K; ++k) lv[k] = ld_stream(a.L + state_off(e0, k, K));
     float w[4] = {0.f, 0.f, 0.f, 0.f}, s = 0.f;
     if (Rh) {
       s = a.S[row * gpr + col0 / a.gs];
