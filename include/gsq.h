@@ -193,8 +193,9 @@ gsq_status gsq_pack(gsq_layer* h, void* packed, size_t packed_bytes, hipStream_t
 gsq_status gsq_get_state(gsq_layer* h, float* logits, float* m, float* v, float* scales,
                          float* m_s, float* v_s, uint8_t* base, int64_t* t, hipStream_t stream);
 
-/* Overwrite the state (same layouts; NULL leaves that part unchanged; t >= 0; every base
- * index must be < n_levels, which the kernels do not check). */
+/* Overwrite the state (same layouts; NULL leaves that part unchanged; t >= 0).  Every base
+ * index should be < n_levels: the kernels read a larger one as n_levels - 1.  Invalid
+ * arguments return before anything is enqueued. */
 gsq_status gsq_set_state(gsq_layer* h, const float* logits, const float* m, const float* v,
                          const float* scales, const float* m_s, const float* v_s,
                          const uint8_t* base, int64_t t, hipStream_t stream);

@@ -467,9 +467,9 @@ gsq_status gsq_set_state(gsq_layer* h, const float* logits, const float* m, cons
   if (t < 0 || t >= (int64_t)UINT32_MAX) return fail(GSQ_EINVAL, "t out of range");
   gsq::Layer& L = *h;
   if (base && !L.J0) return fail(GSQ_EINVAL, "base indices exist only for the SHIFT relaxation");
-  if (base) GSQ_HIP(hipMemcpyAsync(L.J0, base, (size_t)L.N, hipMemcpyDeviceToDevice, stream));
   if (scales && L.cfg.layout == GSQ_LAYOUT_SUPERBLOCK)
     return fail(GSQ_EUNSUPPORTED, "SUPERBLOCK scales are fixed by their 6-bit encoding");
+  if (base) GSQ_HIP(hipMemcpyAsync(L.J0, base, (size_t)L.N, hipMemcpyDeviceToDevice, stream));
   if (logits) GSQ_HIP(gsq::launch_state_io(L, const_cast<float*>(logits), L.L, true, stream));
   if (m) GSQ_HIP(gsq::launch_state_io(L, const_cast<float*>(m), L.M, true, stream));
   if (v) GSQ_HIP(gsq::launch_state_io(L, const_cast<float*>(v), L.V, true, stream));

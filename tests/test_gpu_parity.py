@@ -286,6 +286,13 @@ def test_superblock_rejects_scale_training(dev):
     with pytest.raises(B.GsqError) as e:
         pair.layer.step(B.StepParams(tau=0.5, lr_scales=1e-5))
     assert e.value.status == B.GSQ_EUNSUPPORTED
+    # nor can the scales be overwritten; the rejected call leaves the logits as they were
+    before = pair.get()
+    junk = torch.full((1, 16, 256, 8), 7.0, device=dev)
+    with pytest.raises(B.GsqError) as e:
+        pair.layer.set_state(0, logits=junk, scales=torch.ones(1, 16, 16, device=dev))
+    assert e.value.status == B.GSQ_EUNSUPPORTED
+    np.testing.assert_array_equal(pair.get().logits, before.logits)
 
 
 # ------------------------------------------------------------------ full size, sampled rows
