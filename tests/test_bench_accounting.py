@@ -80,3 +80,14 @@ def test_recorded_backward_traffic_matches_the_algorithmic_bytes():
         assert 0.98 <= r["bytes_per_launch"] / alg <= 1.05, (name, r["bytes_per_launch"], alg)
         checked += 1
     assert checked >= 2
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """The library has no multi-GPU path: --gpus above 1 exits with a message, before any GPU
+    work."""
+    import subprocess
+    import sys
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
