@@ -307,6 +307,27 @@ def test_full_size_layer_on_sampled_rows(dev, name):
     backward pass, loss every step): init and two steps, sampled rows (first, second, interior,
     middle, last) of sampled experts vs the oracle; after the first step, the whole contraction
     of those experts (every element of G) vs the vendor BLAS."""
+    _full_size_steps(dev, name, {}, blas=True)
+
+
+# Lion (the paper's optimiser, Tab. 7's lr 1e-4 and weight decay 1.0) and multi-sample steps
+# (§3.3) at the real shapes
+FULL_SIZE_VARIANTS = [
+    ("attn-4096x4096-k3", dict(optimizer=B.OPT_LION, lr_logits=1e-4, weight_decay=1.0)),
+    ("mlp-down-4096x14336-shift8", dict(optimizer=B.OPT_LION, lr_logits=1e-4, weight_decay=1.0)),
+    ("attn-4096x4096-ternary", dict(samples=3)),
+    ("mlp-up-14336x4096-k8", dict(samples=2)),
+]
+
+
+@pytest.mark.parametrize("name,extra", FULL_SIZE_VARIANTS,
+                         ids=[f"{n}-{'lion' if 'optimizer' in e else 'M%d' % e['samples']}"
+                              for n, e in FULL_SIZE_VARIANTS])
+def test_full_size_lion_and_multi_sample(dev, name, extra):
+    _full_size_steps(dev, name, extra, blas=False)
+
+
+def _full_size_steps(dev, name, extra, blas):
     w = inputs.WORKLOADS[name]
     W, Hd = inputs.make_layer(w, device=dev)
     experts = [0] if w.batch == 1 else [0, 37, w.batch - 1]
@@ -324,7 +345,7 @@ def test_full_size_layer_on_sampled_rows(dev, name):
     layer = B.Layer(pair_cfg, torch.from_numpy(W).to(dev).to(torch.bfloat16), Hd)
     # the library's bf16 H of the sampled experts, (H + H^T) / 2 rounded to nearest even: exactly
     # symmetric, so it serves as the right operand without a transposed view
-    Hs_bf = {e: ((Hd[e] + Hd[e].t()) * 0.5).to(torch.bfloat16) for e in experts}
+    Hs_bf = {e: ((Hd[e] + Hd[e].t()) * 0.5).to(torch.bfloat16) for e in experts} if blas else {}
     torch.cuda.synchronize()
     del Hd                                   # the library keeps its own copy of H
     torch.cuda.empty_cache()
@@ -351,13 +372,13 @@ def test_full_size_layer_on_sampled_rows(dev, name):
     T = w.steps
     for t in range(2):
         tau, nxt = ref.tau_schedule(t, T), ref.tau_schedule(t + 1, T)
-        prm = B.StepParams(tau=tau, tau_next=nxt, lr_scales=w.lr_scales)
+        prm = B.StepParams(tau=tau, tau_next=nxt, lr_scales=w.lr_scales, **extra)
         loss = torch.zeros(Bn, device=dev)
         layer.step(prm, loss_out=loss)
         G = torch.empty(Bn, O, I, device=dev)
-        layer.intermediates(grad=G)
+        layer.intermediates(grad=G)   # of the step's last sample
         G_rows = G[experts][:, rows].cpu().numpy()
-        if t == 0:
+        if blas and t == 0:
             # the whole contraction of the sampled experts against the vendor BLAS (independent
             # code, fp32 accumulation in another order): G = -2 R H in every element
             R = torch.empty(Bn, O, I, dtype=torch.bfloat16, device=dev)
