@@ -191,8 +191,8 @@ def main():
                     help="skip timing the same contraction through the vendor BLAS")
     ap.add_argument("--no-fuse", action="store_true", help="do not draw the next sample in the backward pass")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=512)
-    ap.add_argument("--cpu-steps", type=int, default=3)
+    ap.add_argument("--cpu-rows", type=int, default=1024)
+    ap.add_argument("--cpu-steps", type=int, default=6)
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--optimizer", choices=("adam", "lion"), default="adam",
                     help="adam (default) or lion (the paper's optimiser; lr 1e-4, weight decay 1.0)")
