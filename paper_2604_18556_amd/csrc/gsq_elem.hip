@@ -298,14 +298,14 @@ __global__ __launch_bounds__(kBlock) void k_forward(ElemArgs a) {
 // One parameter's optimiser update.  Adam: bias-corrected (step = lr / (1 - b1^n),
 // rbc2 = 1 / sqrt(1 - b2^n)), plus decoupled decay lr wd theta (AdamW).  Lion: the sign of
 // b1 m + (1 - b1) d, plus decoupled decay; the moment then moves with b2; v is untouched.
-template <bool kF64>
-__device__ __forceinline__ void opt_update(bool lion, Real<kF64> d, Real<kF64>& th, Real<kF64>& m,
+template <bool kF64, bool kLion>
+__device__ __forceinline__ void opt_update(Real<kF64> d, Real<kF64>& th, Real<kF64>& m,
                                            Real<kF64>& v, Real<kF64> lr, Real<kF64> step,
                                            Real<kF64> b1, Real<kF64> b2, Real<kF64> omb1,
                                            Real<kF64> omb2, Real<kF64> rbc2, Real<kF64> eps,
                                            Real<kF64> wd) {
   using T = Real<kF64>;
-  if (lion) {
+  if constexpr (kLion) {
     const T c = b1 * m + omb1 * d;
     const T sg = (T)((c > T(0)) - (c < T(0)));
     th = th - lr * (sg + wd * th);
@@ -373,7 +373,7 @@ constexpr int backward_min_blocks() {
   return (kMode == GSQ_RELAX_GRID && K == 8 && !kScales && !kF64 && !kMulti) ? 3 : 1;
 }
 
-template <int K, bool kF64, bool kScales, bool kMulti, int kMode>
+template <int K, bool kF64, bool kScales, bool kMulti, int kMode, bool kLion>
 __global__ __launch_bounds__(kBlock, (backward_min_blocks<K, kF64, kScales, kMulti, kMode>())) void k_backward(
     ElemArgs a) {
   using T = Real<kF64>;
@@ -390,7 +390,7 @@ __global__ __launch_bounds__(kBlock, (backward_min_blocks<K, kF64, kScales, kMul
   const T step_l = kF64 ? (T)a.step_l_d : (T)a.step_l;
   const T rbc2 = kF64 ? (T)a.rbc2_d : (T)a.rbc2;
   const T lr = (T)a.lr, wd = (T)a.wd;
-  const bool lion = a.lion != 0;
+  constexpr bool lion = kLion;
   const int lpg = a.gs / 4;   // lanes per scale group
   const int64_t gpr = a.I / a.gs;
   bool bad = false;
@@ -468,7 +468,7 @@ __global__ __launch_bounds__(kBlock, (backward_min_blocks<K, kF64, kScales, kMul
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           T th = (T)f4get(lv[k], q), m1 = (T)f4get(mk, q), v1 = (T)f4get(vk, q);
-          opt_update<kF64>(lion, dacc[q][k], th, m1, v1, lr, step_l, b1, b2, omb1, omb2, rbc2,
+          opt_update<kF64, kLion>(dacc[q][k], th, m1, v1, lr, step_l, b1, b2, omb1, omb2, rbc2,
                            eps, wd);
           f4set(mk, q, (float)m1);
           f4set(vk, q, (float)v1);
@@ -496,7 +496,7 @@ __global__ __launch_bounds__(kBlock, (backward_min_blocks<K, kF64, kScales, kMul
 #pragma unroll
         for (int k = 0; k < K; ++k) {
           T th = (T)f4get(lv[k], q), m1 = (T)f4get(mv[k], q), v1 = (T)f4get(vv[k], q);
-          opt_update<kF64>(lion, dacc[q][k], th, m1, v1, lr, step_l, b1, b2, omb1, omb2, rbc2,
+          opt_update<kF64, kLion>(dacc[q][k], th, m1, v1, lr, step_l, b1, b2, omb1, omb2, rbc2,
                            eps, wd);
           f4set(mv[k], q, (float)m1);
           f4set(vv[k], q, (float)v1);
@@ -521,7 +521,7 @@ __global__ __launch_bounds__(kBlock, (backward_min_blocks<K, kF64, kScales, kMul
       if (leader) {
         const T step_s = kF64 ? (T)a.step_s_d : (T)a.step_s;
         T th = s, m1 = (T)a.MS[sidx], v1 = (T)a.VS[sidx];
-        opt_update<kF64>(lion, ds_part, th, m1, v1, (T)a.lr_s, step_s, b1, b2, omb1, omb2, rbc2,
+        opt_update<kF64, kLion>(ds_part, th, m1, v1, (T)a.lr_s, step_s, b1, b2, omb1, omb2, rbc2,
                          eps, wd);
         s_new = (float)th;
         bad |= !(__builtin_isfinite(s_new) && __builtin_isfinite((float)v1));
@@ -972,22 +972,27 @@ hipError_t launch_forward(const Layer& L, const ElemArgs& a, hipStream_t s) {
   }
 }
 
-template <int K, bool kMulti, int kMode>
+template <int K, bool kMulti, int kMode, bool kLion>
 static void backward_km(const Layer& L, const ElemArgs& a, bool sc, hipStream_t s) {
   const dim3 g = row_grid(L), b(kBlock);
   if (L.bf16) {
-    if (sc) hipLaunchKernelGGL((k_backward<K, false, true, kMulti, kMode>), g, b, 0, s, a);
-    else hipLaunchKernelGGL((k_backward<K, false, false, kMulti, kMode>), g, b, 0, s, a);
+    if (sc) hipLaunchKernelGGL((k_backward<K, false, true, kMulti, kMode, kLion>), g, b, 0, s, a);
+    else hipLaunchKernelGGL((k_backward<K, false, false, kMulti, kMode, kLion>), g, b, 0, s, a);
   } else {
-    if (sc) hipLaunchKernelGGL((k_backward<K, true, true, kMulti, kMode>), g, b, 0, s, a);
-    else hipLaunchKernelGGL((k_backward<K, true, false, kMulti, kMode>), g, b, 0, s, a);
+    if (sc) hipLaunchKernelGGL((k_backward<K, true, true, kMulti, kMode, kLion>), g, b, 0, s, a);
+    else hipLaunchKernelGGL((k_backward<K, true, false, kMulti, kMode, kLion>), g, b, 0, s, a);
   }
 }
 
 template <int K, int kMode = GSQ_RELAX_GRID>
 static hipError_t backward_k(const Layer& L, const ElemArgs& a, bool sc, hipStream_t s) {
-  if (a.samples > 1) backward_km<K, true, kMode>(L, a, sc, s);
-  else backward_km<K, false, kMode>(L, a, sc, s);
+  if (a.lion) {
+    if (a.samples > 1) backward_km<K, true, kMode, true>(L, a, sc, s);
+    else backward_km<K, false, kMode, true>(L, a, sc, s);
+  } else {
+    if (a.samples > 1) backward_km<K, true, kMode, false>(L, a, sc, s);
+    else backward_km<K, false, kMode, false>(L, a, sc, s);
+  }
   return hipGetLastError();
 }
 
