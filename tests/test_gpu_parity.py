@@ -404,7 +404,47 @@ def _full_size_steps(dev, name, extra, blas):
         lv = loss.cpu().numpy()
         assert np.all(np.isfinite(lv)) and np.all(lv > 0)
         st = st_new
+    if blas:
+        _check_full_size_harden_and_pack(dev, layer, w, pair_cfg, rcfg, st, gst, experts, rows)
     layer.destroy()
+
+
+def _check_full_size_harden_and_pack(dev, layer, w, pair_cfg, rcfg, st, gst, experts, rows):
+    """gsq_harden and gsq_pack on the whole layer: the codes of the sampled rows are the
+    oracle's hardening of the layer's own logits for those rows, and those rows' bytes in the
+    packed output are the oracle packer's (64-bit offsets: the MoE stream spans 2.8e9 bits)."""
+    Bn, O, I, n = w.batch, w.out_features, w.in_features, len(w.levels)
+    gst.base = st.base
+    c_ref = ref.hard_codes(rcfg, gst)
+    codes = torch.empty(Bn, O, I, dtype=torch.uint8, device=dev)
+    layer.harden(codes=codes)
+    c_gpu = np.stack([codes[e].cpu().numpy()[rows] for e in experts])
+    del codes
+    np.testing.assert_array_equal(c_gpu, c_ref)
+    packed = torch.empty(B.packed_size(pair_cfg), dtype=torch.uint8, device=dev)
+    layer.pack(packed)
+    pk = packed.cpu().numpy()
+    del packed
+    sel = [(e * O + r) for e in experts for r in rows]   # global rows, in c_ref's order
+    if w.layout == "group":
+        b = refpack.code_bits(n)
+        rb, gb = I * b // 8, (I // w.group_size) * 2
+        expect = refpack.pack_plain(c_ref, ref.scales_fp16(gst.scales), n, w.group_size)
+        ncode = len(sel) * rb
+        for j, g in enumerate(sel):
+            np.testing.assert_array_equal(pk[g * rb:(g + 1) * rb], expect[j * rb:(j + 1) * rb])
+            off = Bn * O * rb + g * gb
+            np.testing.assert_array_equal(pk[off:off + gb], expect[ncode + j * gb:ncode + (j + 1) * gb])
+    elif w.layout == "superblock":
+        rb = I // 256 * 110
+        expect = refpack.pack_superblock(c_ref, st.sb_d, st.sb_sc)
+        for j, g in enumerate(sel):
+            np.testing.assert_array_equal(pk[g * rb:(g + 1) * rb], expect[j * rb:(j + 1) * rb])
+    else:   # base-3: rows do not start on byte boundaries, so the whole stream is decoded
+        c_all, s_all = refpack.unpack_base3(pk, Bn, O, I, w.group_size)
+        np.testing.assert_array_equal(np.stack([c_all[e][rows] for e in experts]), c_ref)
+        np.testing.assert_array_equal(np.stack([s_all[e][rows] for e in experts]),
+                                      ref.scales_fp16(gst.scales))
 
 
 # ------------------------------------------------------------------ Lion (§3.3) and AdamW (App. B)
