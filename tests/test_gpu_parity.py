@@ -262,6 +262,40 @@ def test_determinism_and_exact_resume(dev):
     assert sd.t == sa.t == 10
 
 
+def test_calls_on_a_side_stream(dev):
+    """Every call enqueues on the caller's stream: a layer initialised, stepped, read and
+    hardened on a non-default stream matches one driven on the default stream bit for bit."""
+    W, H = layer_inputs(96, 384, seed=12)
+    rcfg = ref.Config(96, 384, L8, 64, precision="bf16", seed=5)
+    a = Pair(rcfg, W, H, dev)
+    wt = torch.from_numpy(a.W).to(dev).to(torch.bfloat16)
+    ht = torch.from_numpy(a.H).to(dev)
+    la, lb = torch.zeros(1, device=dev), torch.zeros(1, device=dev)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    b = B.Layer(a.bcfg, wt, ht, stream=side)
+    losses_a, losses_b = [], []
+    for t in range(6):
+        p = B.StepParams(tau=1.0 - 0.1 * t, tau_next=1.0 - 0.1 * (t + 1), lr_scales=5e-5)
+        a.layer.step(p, loss_out=la)
+        b.step(p, loss_out=lb, stream=side)
+        losses_a.append(la.clone())
+        with torch.cuda.stream(side):
+            losses_b.append(lb.clone())
+    lg = torch.empty(1, 96, 384, 8, device=dev)
+    ca, cb = (torch.empty(1, 96, 384, dtype=torch.uint8, device=dev) for _ in range(2))
+    a.layer.harden(codes=ca)
+    b.get_state(logits=lg, stream=side)
+    b.harden(codes=cb, stream=side)
+    side.synchronize()
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(lg.cpu().numpy(), a.get().logits)
+    np.testing.assert_array_equal(cb.cpu().numpy(), ca.cpu().numpy())
+    np.testing.assert_array_equal(torch.stack(losses_b).cpu().numpy(),
+                                  torch.stack(losses_a).cpu().numpy())
+    b.destroy()
+
+
 # ------------------------------------------------------------------ failure reporting
 def test_non_finite_weights_are_reported(dev):
     W, H = layer_inputs(32, 256, seed=1)
