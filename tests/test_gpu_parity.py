@@ -533,6 +533,52 @@ def test_lion_tiny_layer_trajectory(dev):
     assert rel_err(got.logits, st.logits) <= 1e-5
 
 
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_paper_settings_trajectory(dev, prec):
+    """The paper's own settings (Tab. 7): Lion with lr 1e-4 and weight decay 1.0, logits
+    initialised at sigma_init = 0.01, kappa raised linearly from 100 to 500 while tau falls
+    linearly from 2 to 0.05. 100 steps on the fp32 tiny layer, 60 on a ragged bf16 layer with
+    8 levels: the loss agrees every step, and the codes at the end (except at near ties)."""
+    if prec == "fp32":
+        w = inputs.WORKLOADS["tiny-256x256-k4"]
+        W, H = inputs.make_layer(w)
+        rcfg = ref.Config(256, 256, w.levels, 128, precision="fp32", seed=0, sigma_init=0.01)
+        T, tol = 100, 1e-5
+    else:
+        W, H = layer_inputs(130, 512, seed=17)
+        rcfg = ref.Config(130, 512, L8, 64, precision="bf16", seed=3, sigma_init=0.01)
+        T, tol = 60, 1e-3
+    pair = Pair(rcfg, W, H, dev)
+    st = ref.init_layer(rcfg, W)
+    pair.put(st)
+    kap = lambda t: 100.0 + 400.0 * t / (T - 1)          # noqa: E731
+    tau = lambda t: ref.tau_schedule(t, T, tau0=2.0)      # noqa: E731
+    for t in range(T):
+        last = t + 1 == T
+        prm = B.StepParams(tau=tau(t), kappa=kap(t), lr_logits=1e-4, lr_scales=5e-5,
+                           optimizer=B.OPT_LION, weight_decay=1.0,
+                           tau_next=0.0 if last else tau(t + 1), kappa_next=1.0 if last else kap(t + 1))
+        lg = pair.step(prm)[0]
+        st, L = ref.step(rcfg, W, pair.Hs, st, oracle_params(prm))
+        assert abs(lg - L[0]) <= tol * abs(L[0]), (t, lg, L[0])
+    got = pair.get()
+    diff = np.argwhere(ref.harden(got.logits) != ref.harden(st.logits))
+    srt = np.sort(st.logits, -1)
+    for idx in diff:
+        assert (srt[..., -1] - srt[..., -2])[tuple(idx)] < 1e-4 * np.abs(st.logits).max(), idx
+    if prec == "fp32":
+        assert rel_err(got.logits, st.logits) <= tol
+    else:
+        # Lion moves every logit by lr (sign of its momentum) plus decay each step, whatever the
+        # gradient's size, so where the momentum is within rounding of zero the two runs can
+        # step apart by 2 lr at that step; such coordinates must stay rare
+        d = np.abs(got.logits.astype(np.float64) - st.logits)
+        far = np.mean(d > 4 * 1e-4)
+        print(f"bf16 Lion run: max |dl| {d.max():.2e}, {far:.2e} of logits beyond 4 lr")
+        # (the decay term lr wd l adds at most a quarter on these logits' magnitudes)
+        assert d.max() <= 1.25 * 2 * 1e-4 * T and far < 1e-3
+
+
 @pytest.mark.parametrize("prec,O,I,K,gs,M", [
     ("fp32", 256, 256, 4, 128, 2),
     ("fp32", 70, 384, 3, 64, 3),
