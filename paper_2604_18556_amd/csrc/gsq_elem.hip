@@ -358,23 +358,19 @@ __device__ __forceinline__ double wave_sum_to_lane63(double x) {
 // block (R rebuilt exactly as the contraction saw it) into a.loss_part.
 // Register budget of the backward.  Updating the moments one logit plane at a time (each
 // plane's m and v loaded just before its update) keeps 8K fewer registers live than loading
-// them all first, at the price of less memory parallelism within a wavefront.  It pays only
-// where it buys another wavefront per SIMD: the shift relaxation (2 -> 3 wavefronts, 5 % faster
-// at 4096 x 14336), grids of 5 to 7 levels (2 -> 3), and the 8-level grid with frozen scales
-// under a bound of three wavefronts in the one-sample bf16 path (2 % faster on the super-block
-// MoE).  With trained scales the 8-level grid would spill under that bound (3 % slower); it and
-// the smaller grids keep all moments in flight at once.
-template <int K, bool kScales, int kMode>
+// them all first, at the price of less memory parallelism within a wavefront.  It pays where
+// it buys another wavefront per SIMD: the shift relaxation (2 -> 3 wavefronts, 5 % faster at
+// 4096 x 14336) and grids of 5 to 7 levels (2 -> 3).  The 8-level grids keep every moment in
+// flight at two wavefronts: with the non-temporal state accesses this is 1 % faster on the
+// super-block MoE than the plane-by-plane update under a bound of three wavefronts, and with
+// trained scales that bound spills.  The smaller grids keep all moments in flight as well.
+template <int K, int kMode>
 constexpr bool backward_plane_update() {
-  return kMode == GSQ_RELAX_SHIFT || (kMode == GSQ_RELAX_GRID && K >= 5 && !(K == 8 && kScales));
-}
-template <int K, bool kF64, bool kScales, bool kMulti, int kMode>
-constexpr int backward_min_blocks() {
-  return (kMode == GSQ_RELAX_GRID && K == 8 && !kScales && !kF64 && !kMulti) ? 3 : 1;
+  return kMode == GSQ_RELAX_SHIFT || (kMode == GSQ_RELAX_GRID && K >= 5 && K <= 7);
 }
 
 template <int K, bool kF64, bool kScales, bool kMulti, int kMode, bool kLion>
-__global__ __launch_bounds__(kBlock, (backward_min_blocks<K, kF64, kScales, kMulti, kMode>())) void k_backward(
+__global__ __launch_bounds__(kBlock) void k_backward(
     ElemArgs a) {
   using T = Real<kF64>;
   constexpr int Z = noise_count<K, kMode>();
@@ -458,7 +454,7 @@ __global__ __launch_bounds__(kBlock, (backward_min_blocks<K, kF64, kScales, kMul
     }
     // the moments are needed only by the update: loading them here keeps them out of the
     // registers of the sample loop
-    if constexpr (backward_plane_update<K, kScales, kMode>()) {
+    if constexpr (backward_plane_update<K, kMode>()) {
 #pragma unroll
       for (int k = 0; k < K; ++k) {
         float4 mk = active ? ld_stream(a.M + state_off(e0, k, K))
