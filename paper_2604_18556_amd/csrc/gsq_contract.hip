@@ -278,6 +278,10 @@ __global__ __launch_bounds__(256, 1) void k_contract_bf16(const uint16_t* __rest
 }
 
 // G = -2 (P_0 + ... + P_{split-1}) for the split tiles of the last round, parts added in order.
+// Block (q, y) covers rows y * FIX_ROWS .. of split tile q, so the fixup spreads over enough
+// workgroups to stream at the HBM rate.
+constexpr int FIX_ROWS = 32;
+
 __global__ __launch_bounds__(256) void k_contract_fixup(const float* __restrict__ ws,
                                                         float* __restrict__ G, int64_t Ipad,
                                                         int tiles_m, int tiles_n, Split sp) {
@@ -286,7 +290,8 @@ __global__ __launch_bounds__(256) void k_contract_fixup(const float* __restrict_
   tile_at(sp.full + q, tiles_m, tiles_n, tm, tn);
   const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
   const float* src = ws + (int64_t)q * sp.split * (BM * BN);
-  for (int e = threadIdx.x * 4; e < BM * BN; e += 256 * 4) {
+  const int lo = blockIdx.y * FIX_ROWS * BN, hi = lo + FIX_ROWS * BN;
+  for (int e = lo + threadIdx.x * 4; e < hi; e += 256 * 4) {
     float4 acc = *reinterpret_cast<const float4*>(src + e);
     for (int p = 1; p < sp.split; ++p) {
       const float4 v = *reinterpret_cast<const float4*>(src + (int64_t)p * (BM * BN) + e);
@@ -436,7 +441,7 @@ hipError_t launch_contract(const Layer& L, const void* R, bool want_loss, int sl
     if (sp.split > 1) {
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
-      hipLaunchKernelGGL(k_contract_fixup, dim3((unsigned)(tiles - sp.full)), dim3(256), 0, s,
+      hipLaunchKernelGGL(k_contract_fixup, dim3((unsigned)(tiles - sp.full), BM / FIX_ROWS), dim3(256), 0, s,
                          sp.ws, G, L.Ipad, tiles_m, tiles_n, sp);
     }
   } else {
