@@ -5,12 +5,20 @@
     python -m paper_2604_18556_amd.rocprof_summary traffic --fetch F.csv --write W.csv \
         --copy-fetch CF.csv --copy-write CW.csv --copy-bytes N --kernel backward \
         --workload NAME --cmd "..." [--json profiles/traffic.json] > out.txt
+    python -m paper_2604_18556_amd.rocprof_summary mfma COUNTER_CSV --agent AGENT_CSV --cmd "..."
 
 FETCH_SIZE and WRITE_SIZE are in KiB per dispatch.  ``traffic`` scales each by the ratio of
 the known byte count of a plain device copy (bench.py --copy-calibration) to what the same
 counter reports for that copy, and records the HBM bytes per launch of one GSQ kernel,
 together with the SHA-256 of the kernel's source file, into a JSON file that bench.py reads
 (it reports the traffic only while the source is unchanged).
+
+``mfma`` reads one counter pass holding SQ_VALU_MFMA_BUSY_CYCLES, SQ_INSTS_VALU_MFMA_MOPS_BF16 and
+GRBM_GUI_ACTIVE, and gives for the contraction: the clock while the GPU is active
+(GRBM_GUI_ACTIVE per XCC over the dispatch time), the share of those cycles the matrix cores
+are busy (rocprofv3's MfmaUtil), the bf16 flops (512 per MOPS unit) and the rate they make.
+Contractions dispatched after the first harden kernel are gsq_harden's hard-loss ones and are
+listed apart from the step's.
 """
 import argparse
 import collections
@@ -62,6 +70,59 @@ def cmd_pmc(a):
             print(f"{k:<40} {c:<24} {v:>16.3f}  (n={n})")
 
 
+PEAK_BF16_TFLOPS, NOMINAL_GHZ = 2500.0, 2.4   # MI355X dense bf16 matrix peak and its clock
+
+
+def gpu_agent(path):
+    for r in csv.DictReader(open(path)):
+        if r["Agent_Type"] == "GPU":
+            return int(r["Num_Xcc"]), int(r["Simd_Count"])
+    raise SystemExit(f"no GPU agent in {path}")
+
+
+def median(v):
+    v = sorted(v)
+    n = len(v)
+    return v[n // 2] if n % 2 else 0.5 * (v[n // 2 - 1] + v[n // 2])
+
+
+def cmd_mfma(a):
+    n_xcc, n_simd = gpu_agent(a.agent)
+    per, meta = collections.defaultdict(dict), {}
+    for r in csv.DictReader(open(a.csv)):
+        d = int(r["Dispatch_Id"])
+        per[d][r["Counter_Name"]] = float(r["Counter_Value"])
+        meta[d] = (short(r["Kernel_Name"]),
+                   (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9)
+    first_harden = min((d for d, (k, _) in meta.items() if k == "harden"), default=float("inf"))
+    groups = collections.defaultdict(list)
+    for d, (k, t) in sorted(meta.items()):
+        if k == "contract" or "k_contract_fixup" in k:
+            groups[(k if k == "contract" else "fixup", "step" if d < first_harden else "hard loss")].append(d)
+    print(f"# rocprofv3 MFMA counters of the contraction, median over dispatches\n# command: {a.cmd}\n"
+          f"# GPU: {n_xcc} XCCs, {n_simd} SIMDs; peak {PEAK_BF16_TFLOPS:.0f} TFLOP/s bf16 at "
+          f"{NOMINAL_GHZ} GHz\n")
+    print(f"{'kernel':<10} {'calls':<10} {'n':>3} {'us':>9} {'clock_GHz':>10} {'mfma_busy':>10} "
+          f"{'GFLOP':>9} {'TFLOP/s':>8} {'frac':>6} {'frac@clock':>10} {'lds_conflict':>12}")
+    for (k, kind), ds in sorted(groups.items()):
+        us = median([meta[d][1] * 1e6 for d in ds])
+        if k == "fixup":
+            print(f"{k:<10} {kind:<10} {len(ds):>3} {us:>9.1f}")
+            continue
+        ghz = median([per[d]["GRBM_GUI_ACTIVE"] / n_xcc / meta[d][1] / 1e9 for d in ds])
+        busy = median([per[d]["SQ_VALU_MFMA_BUSY_CYCLES"] / (per[d]["GRBM_GUI_ACTIVE"] / n_xcc * n_simd)
+                       for d in ds])
+        gf = median([per[d]["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512 / 1e9 for d in ds])
+        tf = median([per[d]["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512 / meta[d][1] / 1e12 for d in ds])
+        conf = median([per[d].get("SQ_LDS_BANK_CONFLICT", float("nan")) for d in ds])
+        print(f"{k:<10} {kind:<10} {len(ds):>3} {us:>9.1f} {ghz:>10.3f} {busy:>10.3f} {gf:>9.1f} "
+              f"{tf:>8.0f} {tf / PEAK_BF16_TFLOPS:>6.3f} {tf / (PEAK_BF16_TFLOPS * ghz / NOMINAL_GHZ):>10.3f} "
+              f"{conf:>12.0f}")
+    print("\nclock_GHz: GRBM_GUI_ACTIVE per XCC / dispatch time.  mfma_busy: SQ_VALU_MFMA_BUSY_CYCLES / "
+          "(active cycles x SIMDs) (rocprofv3 MfmaUtil).\nfrac: of the nominal peak; frac@clock: of the "
+          "peak at the measured clock.  lds_conflict: SQ_LDS_BANK_CONFLICT cycles per dispatch.")
+
+
 def cmd_traffic(a):
     f = per_kernel_counters(a.fetch)
     w = per_kernel_counters(a.write)
@@ -99,6 +160,10 @@ def main(argv=None):
     p = sub.add_parser("pmc")
     p.add_argument("csv", nargs="+")
     p.add_argument("--cmd", default="")
+    m = sub.add_parser("mfma")
+    m.add_argument("csv")
+    m.add_argument("--agent", required=True)
+    m.add_argument("--cmd", default="")
     t = sub.add_parser("traffic")
     for k in ("fetch", "write", "copy_fetch", "copy_write", "kernel", "workload"):
         t.add_argument("--" + k.replace("_", "-"), dest=k, required=True)
@@ -106,7 +171,7 @@ def main(argv=None):
     t.add_argument("--json")
     t.add_argument("--cmd", default="")
     a = ap.parse_args(argv)
-    {"stats": cmd_stats, "pmc": cmd_pmc, "traffic": cmd_traffic}[a.what](a)
+    {"stats": cmd_stats, "pmc": cmd_pmc, "mfma": cmd_mfma, "traffic": cmd_traffic}[a.what](a)
 
 
 if __name__ == "__main__":
