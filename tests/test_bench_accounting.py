@@ -91,3 +91,61 @@ def test_bench_refuses_more_than_one_gpu():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_recorded_mfma_flops_are_the_algorithmic_flops():
+    """The bf16 flops the matrix-core counters record for one step contraction
+    (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512, in profiles/mfma_contract_*.txt) are exactly the
+    2 O I^2 of P = R H: the kernel does no redundant products."""
+    import glob
+    b = _bench()
+    files = glob.glob(os.path.join(ROOT, "profiles", "mfma_contract_*.txt"))
+    assert files
+    for path in files:
+        name = os.path.basename(path)[len("mfma_contract_"):-len(".txt")]
+        w = inputs.WORKLOADS[name]
+        alg = b.algorithmic_work(w, fused=True, want_loss=True, lr_scales=w.lr_scales)["contract"][1]
+        rows = [ln.split() for ln in open(path) if ln.startswith("contract ")]
+        step = [r for r in rows if r[1] == "step"]
+        assert len(step) == 1, path
+        gflop = float(step[0][6])
+        assert abs(gflop * 1e9 - alg) <= 0.05e9, (name, gflop, alg / 1e9)
+
+
+def test_mfma_summary_arithmetic(tmp_path, capsys):
+    """The MFMA summary on two hand-made dispatches: clock = GRBM_GUI_ACTIVE per XCC over the
+    dispatch time, busy share = busy cycles over (active cycles x SIMDs), flops = 512 per MOPS
+    unit; a contraction after the first harden kernel is listed as a hard-loss one."""
+    from paper_2604_18556_amd import rocprof_summary as rs
+    agent = tmp_path / "agent.csv"
+    agent.write_text("Agent_Type,Num_Xcc,Simd_Count\nCPU,1,0\nGPU,8,1024\n")
+    cc = tmp_path / "cc.csv"
+    lines = ["Dispatch_Id,Kernel_Name,Counter_Name,Counter_Value,Start_Timestamp,End_Timestamp"]
+    t = 0
+
+    def dispatch(d, kernel, dur_ns, counters):
+        nonlocal t
+        for c, v in counters.items():
+            lines.append(f'{d},"{kernel}",{c},{v},{t},{t + dur_ns}')
+        t += dur_ns + 1000
+
+    # 100 us at 2.0 GHz on each of 8 XCCs: 200000 cycles per XCC; half of 1024 SIMDs' cycles busy
+    dispatch(1, "gsq::k_contract_bf16(x)", 100_000,
+             {"GRBM_GUI_ACTIVE": 8 * 200_000, "SQ_VALU_MFMA_BUSY_CYCLES": 0.5 * 200_000 * 1024,
+              "SQ_INSTS_VALU_MFMA_MOPS_BF16": 2 ** 20, "SQ_LDS_BANK_CONFLICT": 0})
+    dispatch(2, "gsq::k_harden<3>(x)", 10_000, {"GRBM_GUI_ACTIVE": 8 * 20_000})
+    dispatch(3, "gsq::k_contract_bf16(x)", 200_000,
+             {"GRBM_GUI_ACTIVE": 8 * 400_000, "SQ_VALU_MFMA_BUSY_CYCLES": 0.25 * 400_000 * 1024,
+              "SQ_INSTS_VALU_MFMA_MOPS_BF16": 2 ** 20, "SQ_LDS_BANK_CONFLICT": 7})
+    cc.write_text("\n".join(lines) + "\n")
+    rs.main(["mfma", str(cc), "--agent", str(agent)])
+    out = {tuple(ln.split()[:2]): ln.split() for ln in capsys.readouterr().out.splitlines()
+           if ln.startswith("contract ")}
+    step, hard = out[("contract", "step")], out[("contract", "hard")]
+    assert step[2] == "1" and float(step[3]) == pytest.approx(100.0)
+    assert float(step[4]) == pytest.approx(2.0) and float(step[5]) == pytest.approx(0.5)
+    gflop = 2 ** 20 * 512 / 1e9
+    assert float(step[6]) == pytest.approx(gflop, abs=0.05)
+    assert float(step[7]) == pytest.approx(gflop / 100e-6 / 1e3, abs=1)      # TFLOP/s
+    # hard-loss row: "contract hard loss n us ..." has one more token before the numbers
+    assert float(hard[6]) == pytest.approx(0.25) and float(hard[5]) == pytest.approx(2.0)
