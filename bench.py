@@ -1,17 +1,21 @@
 #!/usr/bin/env python3
 """GSQ layer-step benchmark on one MI355X.
 
-A step is one full pass of the hot path over one layer: Philox Gumbel noise, the tempered
-softmax sample and residual (Alg. 1), the contraction P = R H with the loss (Eq. 1), the
-gradient of logits and scales, and the Adam update.  The default workload is the 8B-class
-ternary attention projection (W 4096 x 4096, bf16, K = 3 levels {-1, 0, 1}, groups of 128,
-H from 4096 heavy-tailed synthetic tokens), stepped with the paper's linear temperature
-schedule 1.0 -> 0.05 over 500 steps.  Inputs are seeded and synthetic and resident in HBM
-before timing starts.
+A step is one full pass of the hot path over one layer (here: a batch of layers): Philox
+Gumbel noise, the tempered softmax sample and residual (Alg. 1), the contraction P = R H with
+the loss (Eq. 1), the gradient of logits and scales, and the Adam update.  The default
+workload is the largest one that fits one GPU: 64 routed MoE experts of 2048 x 7168, each with
+its own H (7168 x 7168, from Zipf(1.2)-skewed routed token counts), 8 levels
+{+-0.5 .. +-3.5} in 256-weight super-blocks of 16 x 16 with frozen 6-bit sub-block scales
+(the K-quant-style layout of §4.4 and App. E; experts solved independently as in App. G.1),
+stepped with the linear temperature schedule 1.0 -> 0.05 over 200 steps.  Inputs are seeded
+and synthetic and resident in HBM before timing starts.
 
 Prints one JSON line: steps/s, the roofline of the dominant kernel (its duration measured
-with HIP events on the library's stream during the timed steps), and the CPU oracle timed
-on a bounded sample of the same workload.
+with HIP events on the library's stream during the timed steps), the CPU oracle timed on a
+bounded sample of the same workload, and (key "target_layer") the kernel rooflines of a
+short run on the 4096 x 14336 MLP down projection, whose contraction is the matrix-core
+target.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
     python bench.py --copy-calibration   # plain device copy of known size, for PMC scaling
@@ -30,7 +34,8 @@ METRIC = "GSQ steps/sec per layer (fwd+bwd+update) + % HBM / MFMA peak, 1 MI355X
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 PEAK_BF16_TFLOPS = 2500.0      # dense bf16 MFMA
 PEAK_FP64_TFLOPS = 78.6        # fp64 vector (the FP32 precision accumulates in fp64)
-DEFAULT_WORKLOAD = "attn-4096x4096-k3"
+DEFAULT_WORKLOAD = "moe-64x2048x7168-superblock"
+TARGET_LAYER = "mlp-down-4096x14336-k8"   # the layer the matrix-core target names
 ONCE_REPS = 5                  # timed calls of gsq_harden / gsq_pack
 
 
@@ -96,8 +101,28 @@ def measured_traffic(kernel, workload):
     return rec["bytes_per_launch"]
 
 
-def cpu_baseline(w, W, H, rows, steps, lr_scales, opt_kw):
-    """The oracle, untuned, on ``rows`` rows of the layer for ``steps`` steps (host cores)."""
+# Oracle sample size, in coordinates x K^2 per step (its backward forms K x K level differences
+# per coordinate): about 2 s of host work per step on 16 cores.
+CPU_WORK_PER_STEP = 38_000_000
+
+
+def cpu_sample(w, rows=None, experts=None):
+    """(experts, rows per expert) of the oracle's bounded sample of workload ``w``.
+
+    Rows and experts are independent problems given their H, so a sample of them, scaled by
+    the fraction of coordinates it covers, extrapolates to the whole step.  By default the
+    sample holds about CPU_WORK_PER_STEP coordinates x K^2: two experts of a batched workload."""
+    K = {"shift": 5, "ternary": 2}.get(w.relaxation, len(w.levels))
+    n_exp = min(w.batch, 2) if experts is None else max(1, min(experts, w.batch))
+    if rows is None:
+        rows = int(round(CPU_WORK_PER_STEP / (n_exp * w.in_features * K * K)))
+    rows = max(1, min(rows, w.out_features))
+    return n_exp, rows
+
+
+def cpu_baseline(w, W, Hd, rows, experts, steps, lr_scales, opt_kw):
+    """The oracle, untuned, on ``rows`` rows of ``experts`` layers for ``steps`` steps (host
+    cores); only those layers' H leave the GPU."""
     import numpy as np
     from oracle import gsq as ref
     blas = []
@@ -115,21 +140,27 @@ def cpu_baseline(w, W, H, rows, steps, lr_scales, opt_kw):
             cpu_model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), None)
     except OSError:
         pass
-    rcfg = ref.Config(w.out_features, w.in_features, w.levels, w.group_size, batch=w.batch,
+    # the first `experts` layers as a batch of their own: noise indices ((b O) + o) I + i do not
+    # depend on the batch size, so this is the same computation as on the whole batch
+    rcfg = ref.Config(w.out_features, w.in_features, w.levels, w.group_size, batch=experts,
                       layout=w.layout, precision=w.precision, seed=0, relaxation=w.relaxation,
                       alpha=3.0 if w.relaxation == "ternary" else 6.0)
-    sel = np.arange(min(rows, w.out_features))
-    Hs = ref.symmetrize(H)
-    st = ref.init_layer(rcfg, W, rows=sel)
+    sel = np.arange(rows)
+    Ws = W[:experts]
+    Hs = ref.symmetrize(Hd[:experts].cpu().numpy())
+    Hc = ref.to_contraction_precision(rcfg, Hs)
+    st = ref.init_layer(rcfg, Ws, rows=sel)
     t0 = time.perf_counter()
     for t in range(steps):
         prm = ref.StepParams(tau=ref.tau_schedule(t, w.steps), lr_scales=lr_scales, **opt_kw)
-        st, _ = ref.step(rcfg, W, Hs, st, prm, rows=sel)
+        st, _ = ref.step(rcfg, Ws, Hs, st, prm, rows=sel, Hc=Hc)
     sec = (time.perf_counter() - t0) / steps
-    frac = len(sel) / w.out_features
+    frac = (experts * rows) / (w.batch * w.out_features)
+    what = f"{rows} of {w.out_features} rows" + (f" of {experts} of {w.batch} experts" if w.batch > 1 else "")
     return {"value": frac / sec, "unit": "steps/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{len(sel)} of {w.out_features} rows x {steps} steps "
-                      f"({sec:.2f} s/step), scaled to the whole layer by the row fraction",
+            "sample": f"{what} x {steps} steps ({sec:.2f} s/step); extrapolated to the whole "
+                      f"{'batch' if w.batch > 1 else 'layer'} by the coordinate fraction "
+                      f"{frac:.4g} (rows and experts are independent given their H)",
             "cpu_count": os.cpu_count(), "cpu_model": cpu_model, "numpy": np.__version__,
             "blas": blas}
 
@@ -180,6 +211,88 @@ def copy_calibration(dev, gib=1):
                       "ms_per_copy": ms, "copy_GBs": 2 * n * 4 / (ms * 1e-3) / 1e9}))
 
 
+def kernel_table(kern, work, w, steps):
+    """Per-kernel averages of a timed pass (gsq_timing_read over ``steps`` steps) against their
+    rooflines: algorithmic bytes over the HBM peak, or flops over the matrix-core peak."""
+    per_kernel = {}
+    for name, (ms, cnt) in kern.items():
+        if cnt == 0:
+            continue
+        avg = ms / cnt
+        entry = {"launches": cnt, "avg_ms": avg, "ms_per_step": ms / steps}
+        if name in ("forward", "backward"):
+            gbs = work[name][1] / (avg * 1e-3) / 1e9
+            entry.update(bound="hbm", achieved=gbs, peak=PEAK_HBM_GBS, unit="GB/s",
+                         frac=gbs / PEAK_HBM_GBS, bytes_per_launch=work[name][1])
+        elif name == "contract":
+            tf = work[name][1] / (avg * 1e-3) / 1e12
+            peak = PEAK_BF16_TFLOPS if w.precision == "bf16" else PEAK_FP64_TFLOPS
+            entry.update(bound="mfma" if w.precision == "bf16" else "alu", achieved=tf, peak=peak,
+                         unit="TFLOP/s", frac=tf / peak, flops_per_launch=work[name][1])
+        per_kernel[name] = entry
+    return per_kernel
+
+
+KERNEL_SOURCE = {"forward": "gsq_elem.hip", "backward": "gsq_elem.hip", "contract": "gsq_contract.hip"}
+
+
+def dominant_roofline(per_kernel, w):
+    """The roofline object of the kernel with the largest time per step."""
+    dom = max((k for k in per_kernel if "bound" in per_kernel[k]),
+              key=lambda k: per_kernel[k]["ms_per_step"])
+    d = per_kernel[dom]
+    return {"bound": d["bound"], "achieved": d["achieved"], "peak": d["peak"], "unit": d["unit"],
+            "frac": d["frac"], "traffic": measured_traffic(dom, w.name), "kernel": dom,
+            "avg_ms": d["avg_ms"], "source": KERNEL_SOURCE[dom]}
+
+
+def make_config(B, w):
+    return B.LayerConfig(w.out_features, w.in_features, w.levels, w.group_size, w.batch,
+                         {"superblock": B.LAYOUT_SUPERBLOCK, "base3": B.LAYOUT_BASE3}.get(w.layout, B.LAYOUT_GROUP),
+                         B.PREC_BF16 if w.precision == "bf16" else B.PREC_FP32, seed=0,
+                         alpha=3.0 if w.relaxation == "ternary" else 6.0,
+                         relaxation={"shift": B.RELAX_SHIFT, "ternary": B.RELAX_TERNARY}.get(
+                             w.relaxation, B.RELAX_GRID))
+
+
+def tau_at(t, T):
+    """Linear anneal 1.0 -> 0.05 over T steps, the last step at 0.05 (repeats after T)."""
+    t %= T
+    return 1.0 + (0.05 - 1.0) * t / (T - 1)
+
+
+def target_layer(name, dev, steps=10, warmup=3):
+    """Kernel rooflines of a short run (``steps`` timed steps after ``warmup``) on the layer the
+    matrix-core target names: each launch between the library's HIP events on its stream."""
+    import torch
+    from paper_2604_18556_amd import binding as B
+    from paper_2604_18556_amd import inputs
+    w = inputs.WORKLOADS[name]
+    W, Hd = inputs.make_layer(w, device=dev)
+    Wd = torch.from_numpy(W).to(dev).to(torch.bfloat16)
+    layer = B.Layer(make_config(B, w), Wd, Hd)
+    del W, Wd, Hd
+    loss = torch.zeros(w.batch, device=dev)
+    for i in range(warmup + steps):
+        if i == warmup:
+            layer.timing(True)
+            layer.timing_read(reset=True)
+        layer.step(B.StepParams(tau=tau_at(i, w.steps), lr_scales=w.lr_scales,
+                                tau_next=tau_at(i + 1, w.steps)), loss_out=loss)
+    kern = layer.timing_read(reset=True)
+    layer.check()
+    layer.destroy()
+    per_kernel = kernel_table(kern, algorithmic_work(w, True, True, w.lr_scales), w, steps)
+    out = {"workload": name, "steps": steps, "warmup": warmup}
+    for k in ("contract", "backward"):
+        e = per_kernel[k]
+        out[k] = {key: e[key] for key in ("avg_ms", "bound", "achieved", "peak", "unit", "frac")}
+        out[k]["traffic"] = measured_traffic(k, name)
+    out["note"] = ("the contraction's matrix-core fraction (bf16 peak 2.5 PFLOP/s) and the "
+                   "backward's HBM fraction on this layer; steps of the same schedule")
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -191,9 +304,15 @@ def main():
                     help="skip timing the same contraction through the vendor BLAS")
     ap.add_argument("--no-fuse", action="store_true", help="do not draw the next sample in the backward pass")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=1024)
+    ap.add_argument("--cpu-rows", type=int, default=None,
+                    help="rows per sampled layer of the oracle baseline (default: about "
+                         f"{CPU_WORK_PER_STEP:,} coordinates x K^2 per step)")
+    ap.add_argument("--cpu-experts", type=int, default=None,
+                    help="layers of a batched workload in the oracle sample (default 2)")
     ap.add_argument("--cpu-steps", type=int, default=6)
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--target-layer", default=TARGET_LAYER,
+                    help="workload of the short extra run reported under target_layer ('' skips it)")
     ap.add_argument("--optimizer", choices=("adam", "lion"), default="adam",
                     help="adam (default) or lion (the paper's optimiser; lr 1e-4, weight decay 1.0)")
     ap.add_argument("--samples", type=int, default=1,
@@ -221,12 +340,7 @@ def main():
     Wd = torch.from_numpy(W).to(dev)
     if w.precision == "bf16":
         Wd = Wd.to(torch.bfloat16)
-    cfg = B.LayerConfig(w.out_features, w.in_features, w.levels, w.group_size, w.batch,
-                        {"superblock": B.LAYOUT_SUPERBLOCK, "base3": B.LAYOUT_BASE3}.get(w.layout, B.LAYOUT_GROUP),
-                        B.PREC_BF16 if w.precision == "bf16" else B.PREC_FP32, seed=0,
-                        alpha=3.0 if w.relaxation == "ternary" else 6.0,
-                        relaxation={"shift": B.RELAX_SHIFT, "ternary": B.RELAX_TERNARY}.get(
-                            w.relaxation, B.RELAX_GRID))
+    cfg = make_config(B, w)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     layer = B.Layer(cfg, Wd, Hd)
@@ -239,15 +353,11 @@ def main():
     opt_kw = dict(optimizer=B.OPT_LION, lr_logits=1e-4, weight_decay=1.0) if lion else {}
     loss = torch.zeros(w.batch, device=dev)
 
-    def tau_at(t):
-        t %= T
-        return 1.0 + (0.05 - 1.0) * t / (T - 1)
-
     def run(t0, n):
         for i in range(n):
             t = t0 + i
-            p = B.StepParams(tau=tau_at(t), lr_scales=w.lr_scales,
-                             tau_next=tau_at(t + 1) if fused else 0.0, samples=args.samples,
+            p = B.StepParams(tau=tau_at(t, T), lr_scales=w.lr_scales,
+                             tau_next=tau_at(t + 1, T) if fused else 0.0, samples=args.samples,
                              **opt_kw)
             layer.step(p, loss_out=loss if (t % args.loss_every == 0) else None)
 
@@ -291,28 +401,8 @@ def main():
     layer.timing(False)
 
     work = algorithmic_work(w, fused, args.loss_every == 1, w.lr_scales, lion, args.samples)
-    per_kernel = {}
-    for name, (ms, cnt) in kern.items():
-        if cnt == 0:
-            continue
-        avg = ms / cnt
-        entry = {"launches": cnt, "avg_ms": avg, "ms_per_step": ms / args.steps}
-        if name in ("forward", "backward"):
-            gbs = work[name][1] / (avg * 1e-3) / 1e9
-            entry.update(bound="hbm", achieved=gbs, peak=PEAK_HBM_GBS, unit="GB/s",
-                         frac=gbs / PEAK_HBM_GBS, bytes_per_launch=work[name][1])
-        elif name == "contract":
-            tf = work[name][1] / (avg * 1e-3) / 1e12
-            peak = PEAK_BF16_TFLOPS if w.precision == "bf16" else PEAK_FP64_TFLOPS
-            entry.update(bound="mfma" if w.precision == "bf16" else "alu", achieved=tf, peak=peak,
-                         unit="TFLOP/s", frac=tf / peak, flops_per_launch=work[name][1])
-        per_kernel[name] = entry
-    dom = max((k for k in per_kernel if "bound" in per_kernel[k]), key=lambda k: per_kernel[k]["ms_per_step"])
-    d = per_kernel[dom]
-    src = {"forward": "gsq_elem.hip", "backward": "gsq_elem.hip", "contract": "gsq_contract.hip"}[dom]
-    roofline = {"bound": d["bound"], "achieved": d["achieved"], "peak": d["peak"], "unit": d["unit"],
-                "frac": d["frac"], "traffic": measured_traffic(dom, w.name), "kernel": dom,
-                "avg_ms": d["avg_ms"], "source": src}
+    per_kernel = kernel_table(kern, work, w, args.steps)
+    roofline = dominant_roofline(per_kernel, w)
 
     # the step's ideal time: each kernel's algorithmic bytes at the HBM peak, or flops at the
     # matrix-core peak, added (the kernels run one after another)
@@ -333,12 +423,18 @@ def main():
         except (RuntimeError, TypeError) as ex:   # an older torch without out_dtype
             lib_gemm = {"error": str(ex)[:200]}
 
+    layer.destroy()
+    target = None
+    if args.target_layer and args.target_layer != w.name:
+        target = target_layer(args.target_layer, dev)
+
     cpu = None
     if not args.no_cpu_baseline:
         ref_opt = dict(samples=args.samples)
         if lion:
             ref_opt.update(optimizer="lion", lr_logits=1e-4, weight_decay=1.0)
-        cpu = cpu_baseline(w, W, Hd.cpu().numpy(), args.cpu_rows, args.cpu_steps, w.lr_scales, ref_opt)
+        n_exp, rows = cpu_sample(w, args.cpu_rows, args.cpu_experts)
+        cpu = cpu_baseline(w, W, Hd, rows, n_exp, args.cpu_steps, w.lr_scales, ref_opt)
 
     out = {
         "metric": METRIC,
@@ -377,10 +473,10 @@ def main():
                                    "a hard loss); pack: the bit-packing kernels of gsq_pack, which "
                                    "first re-derives the codes (pack_harden_ms)"},
         "library_gemm": lib_gemm,
+        "target_layer": target,
         "gpu_vs_cpu": None if cpu is None else (1e3 / ms_step) / cpu["value"],
     }
     print(json.dumps(out), flush=True)
-    layer.destroy()
 
 
 if __name__ == "__main__":

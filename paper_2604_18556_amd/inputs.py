@@ -64,6 +64,10 @@ WORKLOADS = {
                  8192, 500, "student_t4", True, 5e-5, "shift"),
         Workload("attn-4096x4096-ternary", 1, 1, 4096, 4096, L3, 128, "base3", "bf16",
                  4096, 500, "student_t4", True, 5e-5, "ternary"),
+        # the K-quant experts with the local shift, App. E's relaxation for sets of more than
+        # four values
+        Workload("moe-64x2048x7168-superblock-shift8", 5, 64, 2048, 7168, L8, 16, "superblock",
+                 "bf16", 2048, 200, "student_t4", True, 0.0, "shift"),
     )
 }
 
