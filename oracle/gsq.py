@@ -109,8 +109,9 @@ class Config:
 
     @property
     def n_noise(self):
-        """Gumbel values per coordinate and draw: one per logit of each categorical."""
-        return 4 if self.relaxation == "ternary" else self.K
+        """Noise values per coordinate and draw: one Gumbel value per logit of a categorical,
+        or one logistic value per binary pair (ternary: the mask's, then the sign's)."""
+        return 2 if self.relaxation == "ternary" else self.K
 
     @property
     def gs(self):
@@ -401,9 +402,16 @@ def backward(cfg, G, s_coord, p, v, tau, kappa, cand=None):
     return dlog, dscale
 
 
-def binary_sample(logit, g2, tau, kappa):
-    """Alg. 1 on a two-element set with logits {-l, l} (§3): returns (p_first, p_second)."""
+def binary_sample(logit, d, tau, kappa):
+    """Alg. 1 on a two-element set with logits {-l, l} (§3): returns (p_first, p_second).
+
+    The softmax of (kappa (-l) + g0, kappa l + g1) / tau depends on the two Gumbel values
+    only through d = g1 - g0, a Logistic(0,1) variable; ``d`` is that difference, entered as
+    the noise (0, d) of the two elements.
+    """
     l = np.asarray(logit, np.float64)
+    d = np.asarray(d, np.float64)
+    g2 = np.stack([np.zeros_like(d), d], axis=-1)
     p = soft_sample(np.stack([-l, l], axis=-1), g2, tau, kappa)
     return p[..., 0], p[..., 1]
 
@@ -412,12 +420,13 @@ def ternary_forward(cfg, W, logits, s_coord, g, tau, kappa):
     """Ternary sample of Alg. 2: mask m~ = GS({0, 1}, {-l_m, l_m}), sign
     b~ = GS({-1, 1}, {-l_b, l_b}), W_hat = s m~ b~ (Eq. 2).
 
-    ``logits`` (..., 2) holds (l_m, l_b); ``g`` (..., 4) the Gumbel noise of the mask's two
-    values then of the sign's two.  Returns (p, v, R): p (..., 2, 2) the two pairs of
-    probabilities, v = m~ b~ the soft level, R the residual in the contraction precision.
+    ``logits`` (..., 2) holds (l_m, l_b); ``g`` (..., 2) the logistic noise of the mask pair
+    then of the sign pair (each the difference of the pair's two Gumbel values, see
+    ``binary_sample``).  Returns (p, v, R): p (..., 2, 2) the two pairs of probabilities,
+    v = m~ b~ the soft level, R the residual in the contraction precision.
     """
-    p0m, p1m = binary_sample(logits[..., 0], g[..., 0:2], tau, kappa)
-    p0b, p1b = binary_sample(logits[..., 1], g[..., 2:4], tau, kappa)
+    p0m, p1m = binary_sample(logits[..., 0], g[..., 0], tau, kappa)
+    p0b, p1b = binary_sample(logits[..., 1], g[..., 1], tau, kappa)
     m = p1m                                  # 0 * p0 + 1 * p1
     b = p1b - p0b                            # -1 * p0 + 1 * p1
     v = m * b
@@ -527,7 +536,9 @@ def step(cfg, W, Hs, st, prm, rows=None, want=False, batches=None, Hc=None):
         nz = cfg.n_noise
         dlog = dsc = 0.0
         for smp in range(prm.samples):
-            if prm.gumbel_noise:
+            if prm.gumbel_noise and cfg.relaxation == "ternary":
+                g = philox.logistic(cfg.seed, e, st.t, nz, smp).reshape(len(rows), I, nz)
+            elif prm.gumbel_noise:
                 g = philox.gumbel(cfg.seed, e, st.t, nz, smp).reshape(len(rows), I, nz)
             else:
                 g = np.zeros((len(rows), I, nz))

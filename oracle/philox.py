@@ -21,7 +21,9 @@ Counter layout (a reading of ours, stated once here):
 
 Pinned by: rocRAND's host Philox4x32-10 (tests/test_oracle_rng.py), chi-square
 uniformity, Gumbel moments (mean = Euler-Mascheroni constant, variance pi^2/6),
-and the Gumbel-max property (argmax(l + g) ~ softmax(l)).
+the Gumbel-max property (argmax(l + g) ~ softmax(l)), and for the logistic
+values of the binary relaxations: moments (0, pi^2/3), the logistic CDF, and
+the law of a difference of two of the generator's Gumbel values.
 """
 import numpy as np
 
@@ -107,6 +109,20 @@ def gumbel(seed, e, t, n_levels, sample=0):
     """
     u = uniform(raw_words(seed, e, t, STREAM_STEP, n_levels, sample))
     return np.float32(-np.log(-np.log(u))).astype(np.float64)
+
+
+def logistic(seed, e, t, n_values, sample=0):
+    """Logistic(0,1) noise d = ln u - ln(1 - u), evaluated in float64, stored as float32.
+
+    A two-element Gumbel-Softmax with logits {-l, l} (§3) sees its two Gumbel draws only
+    through their difference g1 - g0, and the difference of two independent Gumbel(0,1)
+    variables is Logistic(0,1); so the binary relaxations draw that difference directly, one
+    value per pair (reading), from the same word stream and chunk layout as ``gumbel``.
+    1 - u is exact for every u of ``uniform``.  Returns float64 values that are exactly
+    float32-representable, shape (len(e), n_values).
+    """
+    u = uniform(raw_words(seed, e, t, STREAM_STEP, n_values, sample))
+    return np.float32(np.log(u) - np.log(1.0 - u)).astype(np.float64)
 
 
 def init_normals(seed, e, n_levels):

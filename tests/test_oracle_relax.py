@@ -166,31 +166,45 @@ def test_shift_init_is_the_centred_prior_around_the_rtn_code():
 # ------------------------------------------------------------------ ternary mask x sign
 def test_ternary_pairs_are_sigmoids_of_twice_the_logit():
     """§3: a two-element GS with logits {-l, l} is a sigmoid of the noisy logit 2l, so the mask
-    is sigmoid((2 kappa l_m + g1 - g0) / tau) and the sign 2 sigmoid(...) - 1."""
+    is sigmoid((2 kappa l_m + d_m) / tau) and the sign 2 sigmoid(...) - 1, d the pair's
+    logistic noise (the difference of its two Gumbel values)."""
     rng = np.random.default_rng(40)
     n = 2000
     lg = rng.standard_normal((1, n, 2)) * 2
-    g = philox.gumbel(3, np.arange(n), 4, 4).reshape(1, n, 4)
+    d = philox.logistic(3, np.arange(n), 4, 2).reshape(1, n, 2)
     cfg = gsq.Config(1, n, L3, 16 if n % 16 == 0 else 1, precision="fp64", relaxation="ternary")
     for tau, kappa in ((1.0, 1.0), (0.2, 3.0)):
-        p, v, _ = gsq.ternary_forward(cfg, np.zeros((1, n)), lg, np.ones((1, n)), g, tau, kappa)
-        m = expit((2 * kappa * lg[..., 0] + g[..., 1] - g[..., 0]) / tau)
-        b = 2 * expit((2 * kappa * lg[..., 1] + g[..., 3] - g[..., 2]) / tau) - 1
+        p, v, _ = gsq.ternary_forward(cfg, np.zeros((1, n)), lg, np.ones((1, n)), d, tau, kappa)
+        m = expit((2 * kappa * lg[..., 0] + d[..., 0]) / tau)
+        b = 2 * expit((2 * kappa * lg[..., 1] + d[..., 1]) / tau) - 1
         np.testing.assert_allclose(p[..., 0, 1], m, rtol=1e-12, atol=1e-300)
         np.testing.assert_allclose(v, m * b, rtol=1e-10, atol=1e-15)
 
 
+def test_ternary_pair_with_two_gumbels_equals_the_pair_with_their_difference():
+    """Alg. 1 on {-l, l} with Gumbel values (g0, g1) gives the same probabilities as the pair
+    driven by the single value d = g1 - g0 (the softmax sees only the difference)."""
+    rng = np.random.default_rng(46)
+    n = 3000
+    l = rng.standard_normal(n) * 2
+    g = philox.gumbel(8, np.arange(n), 2, 2)
+    for tau, kappa in ((1.0, 1.0), (0.1, 2.5)):
+        full = gsq.soft_sample(np.stack([-l, l], -1), g, tau, kappa)
+        p0, p1 = gsq.binary_sample(l, g[:, 1] - g[:, 0], tau, kappa)
+        np.testing.assert_allclose(p1, full[:, 1], rtol=1e-12, atol=1e-300)
+        np.testing.assert_allclose(p0, full[:, 0], rtol=1e-12, atol=1e-300)
+
+
 def test_ternary_mask_frequency_is_the_logistic_of_twice_the_logit():
-    """The difference of two independent Gumbel(0,1) draws is logistic, so at tau -> 0 the mask is
-    1 with probability sigmoid(2 kappa l) (checked with the generator's own noise)."""
+    """The mask's noise is logistic, so at tau -> 0 the mask is 1 with probability
+    sigmoid(2 kappa l) (checked with the generator's own noise), for the mask and the sign."""
     n = 200_000
-    g = philox.gumbel(9, np.arange(n), 7, 4)
+    d = philox.logistic(9, np.arange(n), 7, 2)
     for l, kappa in ((0.3, 1.0), (-0.8, 0.5)):
-        frac = np.mean(2 * kappa * l + g[:, 1] - g[:, 0] > 0)
         p = expit(2 * kappa * l)
-        assert abs(frac - p) < 5 * math.sqrt(p * (1 - p) / n)
-        fb = np.mean(2 * kappa * l + g[:, 3] - g[:, 2] > 0)
-        assert abs(fb - p) < 5 * math.sqrt(p * (1 - p) / n)
+        for j in (0, 1):
+            frac = np.mean(2 * kappa * l + d[:, j] > 0)
+            assert abs(frac - p) < 5 * math.sqrt(p * (1 - p) / n)
 
 
 def test_ternary_low_temperature_limit():
@@ -199,9 +213,9 @@ def test_ternary_low_temperature_limit():
     n = 512
     cfg = gsq.Config(1, n, L3, 16, precision="fp64", relaxation="ternary")
     lg = rng.standard_normal((1, n, 2))
-    g = philox.gumbel(5, np.arange(n), 3, 4).reshape(1, n, 4)
-    _, v, _ = gsq.ternary_forward(cfg, np.zeros((1, n)), lg, np.ones((1, n)), g, 1e-7, 1.0)
-    hard = (2 * lg[..., 0] + g[..., 1] - g[..., 0] > 0) * np.sign(2 * lg[..., 1] + g[..., 3] - g[..., 2])
+    d = philox.logistic(5, np.arange(n), 3, 2).reshape(1, n, 2)
+    _, v, _ = gsq.ternary_forward(cfg, np.zeros((1, n)), lg, np.ones((1, n)), d, 1e-7, 1.0)
+    hard = (2 * lg[..., 0] + d[..., 0] > 0) * np.sign(2 * lg[..., 1] + d[..., 1])
     np.testing.assert_allclose(v, hard, atol=1e-9)
 
 
@@ -214,7 +228,7 @@ def test_ternary_backward_matches_finite_differences(tau, kappa):
     W = rng.normal(0, 0.02, (O, I))
     lg = rng.standard_normal((O, I, 2))
     sc = rng.uniform(0.01, 0.03, (O, I // gs))
-    g = philox.gumbel(2, np.arange(O * I), 1, 4).reshape(O, I, 4)
+    g = philox.logistic(2, np.arange(O * I), 1, 2).reshape(O, I, 2)
     s_coord = gsq.expand_scales(sc, gs)
     p, v, R = gsq.ternary_forward(cfg, W, lg, s_coord, g, tau, kappa)
     P, _ = gsq.contract(cfg, R, H)
@@ -246,9 +260,10 @@ def test_ternary_backward_matches_torch_autograd_of_alg2():
     lg = rng.standard_normal((O, I, 2))
     sc = rng.uniform(0.01, 0.03, (O, I // gs))
     g = philox.gumbel(1, np.arange(O * I), 0, 4).reshape(O, I, 4)
+    d = np.stack([g[..., 1] - g[..., 0], g[..., 3] - g[..., 2]], -1)
     tau, kappa = 0.4, 1.5
     s_coord = gsq.expand_scales(sc, gs)
-    p, v, R = gsq.ternary_forward(cfg, W, lg, s_coord, g, tau, kappa)
+    p, v, R = gsq.ternary_forward(cfg, W, lg, s_coord, d, tau, kappa)
     P, _ = gsq.contract(cfg, R, H)
     dl, ds = gsq.ternary_backward(cfg, (-2 * P)[None], s_coord[None], p[None], tau, kappa)
     tl = torch.tensor(lg, requires_grad=True)

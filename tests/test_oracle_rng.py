@@ -88,6 +88,37 @@ def test_gumbel_max_samples_the_softmax():
     assert stats.chisquare(np.bincount(k, minlength=5), n * p).pvalue > 1e-4
 
 
+def test_logistic_moments_and_cdf():
+    """Logistic(0,1): mean 0, variance pi^2 / 3, CDF 1 / (1 + e^-x), symmetric."""
+    d = philox.logistic(4, np.arange(400_000, dtype=np.int64), 13, 2).reshape(-1)
+    n = d.size
+    var = np.pi**2 / 3
+    assert abs(d.mean()) < 5 * np.sqrt(var / n)
+    mu4 = (3 + 6 / 5) * var**2                  # excess kurtosis of the logistic: 6/5
+    assert abs(d.var() - var) < 5 * np.sqrt((mu4 - var**2) / n)
+    assert stats.kstest(d[:200_000], stats.logistic.cdf).pvalue > 1e-4
+    # the word -> value map is monotone and antisymmetric under u -> 1 - u (x -> ~x)
+    w = np.array([0, 1 << 9, 0x7FFFFFFF, 0x80000000, 0xFFFFFFFF], dtype=np.uint32)
+    u = philox.uniform(w)
+    val = np.log(u) - np.log(1.0 - u)
+    assert np.all(np.diff(val) >= 0)
+    np.testing.assert_allclose(val + (np.log(1 - u) - np.log(u)), 0.0, atol=0)
+
+
+def test_logistic_has_the_law_of_a_difference_of_two_gumbels():
+    """The binary relaxation's noise replaces g1 - g0 of two independent Gumbel(0,1) values: the
+    generator's logistic values and differences of its Gumbel values have one law (two-sample
+    KS), and the logistic values are the transform ln(u / (1 - u)) of the same words."""
+    g = philox.gumbel(6, np.arange(150_000, dtype=np.int64), 3, 2)
+    d = philox.logistic(6, np.arange(150_000, 300_000, dtype=np.int64), 3, 2).reshape(-1)
+    assert stats.ks_2samp(g[:, 1] - g[:, 0], d).pvalue > 1e-4
+    e = np.arange(1000, dtype=np.int64)
+    u = philox.uniform(philox.raw_words(6, e, 3, philox.STREAM_STEP, 2))
+    want = np.float32(np.log(u / (1 - u))).astype(np.float64)
+    got = philox.logistic(6, e, 3, 2)
+    assert np.abs(got - want).max() <= 2 * np.abs(want).max() * 2.0**-24
+
+
 def test_init_normals_are_standard_normal():
     z = philox.init_normals(2, np.arange(200_000, dtype=np.int64), 8).reshape(-1)
     assert abs(z.mean()) < 5 / np.sqrt(z.size)
