@@ -173,8 +173,11 @@ gsq_status gsq_harden(gsq_layer* h, uint8_t* codes, float* scales, float* hard_l
 size_t gsq_packed_size(const gsq_config* cfg);
 
 /*
- * Pack the hardened layer into `packed` (device, >= gsq_packed_size bytes).
- * GROUP: one little-endian bitstream of b-bit codes (code = level index) over all
+ * Pack the hardened layer into `packed` (device, >= gsq_packed_size bytes, any alignment):
+ * the deployment formats of the quantized weights -- Tab. 1's b-bit codes plus one 16-bit
+ * scale per group (b + 16/gs bits per parameter, ternary at 1.6 + 16/gs), and the
+ * K-quant-style super-blocks of §4.4 and App. E, into which the optimised codes are projected
+ * back.  GROUP: one little-endian bitstream of b-bit codes (code = level index) over all
  * coordinates in row-major order, then the fp16 scales row-major.  BASE3: the codes
  * t in {0, 1, 2} in row-major order, five per byte, byte n = sum_j t_{5n+j} 3^j (the last
  * byte padded with zero codes), then the fp16 scales row-major.  SUPERBLOCK: per
@@ -209,11 +212,14 @@ gsq_status gsq_set_state(gsq_layer* h, const float* logits, const float* m, cons
 gsq_status gsq_get_intermediates(gsq_layer* h, void* residual, float* grad, hipStream_t stream);
 
 /*
- * The Gumbel noise the step kernels draw (Alg. 1): g for the `count` coordinates
- * starting at global index e0 (e = ((b*O)+o)*I + i) at step t, Z values each, into g_out
- * (device fp32, count x Z), Z = the logits per coordinate (GRID: n_levels, SHIFT: 5) or 4
- * for TERNARY (the mask's two values, then the sign's two).  Uses cfg's seed and precision
- * (FP32: -ln(-ln u) evaluated in fp64 and rounded; BF16: hardware log2).
+ * The noise the step kernels draw (Alg. 1): for the `count` coordinates starting at global
+ * index e0 (e = ((b*O)+o)*I + i) at step t, Z values each, into g_out (device fp32,
+ * count x Z).  GRID, SHIFT: Z = the logits per coordinate (n_levels, 5) Gumbel(0,1) values
+ * g = -ln(-ln u).  TERNARY: Z = 2 Logistic(0,1) values d = ln u - ln(1 - u), the mask pair's
+ * then the sign pair's: a two-value relaxation with logits {-l, l} is a sigmoid of
+ * 2 kappa l + g1 - g0 (§3), so each pair draws the difference of its two Gumbel values, which
+ * has this law, as one value.  Uses cfg's seed and precision (FP32: evaluated in fp64 and
+ * rounded once; BF16: hardware log2).
  */
 gsq_status gsq_gumbel(const gsq_config* cfg, int64_t e0, int64_t count, int64_t t, float* g_out,
                       hipStream_t stream);

@@ -157,6 +157,19 @@ def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
+def _arg(t, name, numel, dtypes):
+    """Check a tensor argument before its pointer reaches the library, which reads or writes
+    exactly ``numel`` elements through it: a dense device tensor of one of ``dtypes``."""
+    if t is None:
+        return
+    if not (t.is_cuda and t.is_contiguous()):
+        raise ValueError(f"{name} must be a contiguous device tensor")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name} must be {' or '.join(str(d) for d in dtypes)}, got {t.dtype}")
+    if t.numel() != numel:
+        raise ValueError(f"{name} must hold {numel} elements, got {t.numel()}")
+
+
 def _stream(stream):
     import torch
     s = stream if stream is not None else torch.cuda.current_stream()
@@ -168,7 +181,11 @@ def packed_size(cfg):
 
 
 def gumbel(cfg, e0, count, t, out, stream=None):
-    """Noise of coordinates [e0, e0 + count) at step t into ``out`` (cuda fp32, count x K)."""
+    """Noise of coordinates [e0, e0 + count) at step t into ``out`` (cuda fp32, count x Z):
+    Z = K Gumbel values, or for TERNARY the two pairs' logistic values."""
+    import torch
+    if count > 0:
+        _arg(out, "out", count * cfg.K, (torch.float32,))
     _check(load().gsq_gumbel(ctypes.byref(cfg.to_c()), e0, count, t, _ptr(out), _stream(stream)))
 
 
@@ -191,6 +208,10 @@ class Layer:
                 raise ValueError(f"{name} must be a contiguous device tensor")
         if H.dtype != torch.float32:
             raise TypeError("H must be float32")
+        B, O, I = cfg.batch, cfg.out_features, cfg.in_features
+        _arg(W, "W", B * O * I, (torch.float32, torch.bfloat16))
+        _arg(H, "H", B * I * I, (torch.float32,))
+        _arg(scales_init, "scales_init", B * O * (I // cfg.gs), (torch.float32,))
         h = ctypes.c_void_p()
         _check(lib.gsq_layer_init(ctypes.byref(self._c), _ptr(W), wdt, _ptr(H), _ptr(scales_init),
                                   _stream(stream), ctypes.byref(h)))
@@ -202,20 +223,40 @@ class Layer:
             raise RuntimeError("layer destroyed")
         return self._h
 
+    # element counts of the caller-side tensors
+    @property
+    def _n(self):
+        c = self.cfg
+        return c.batch * c.out_features * c.in_features
+
+    @property
+    def _ng(self):
+        c = self.cfg
+        return c.batch * c.out_features * (c.in_features // c.gs)
+
     def step(self, params, loss_out=None, stream=None):
+        import torch
+        _arg(loss_out, "loss_out", self.cfg.batch, (torch.float32,))
         _check(load().gsq_step(self.handle, ctypes.byref(params.to_c()), _ptr(loss_out),
                                _stream(stream)))
 
     def harden(self, codes=None, scales=None, hard_loss=None, stream=None):
+        import torch
+        _arg(codes, "codes", self._n, (torch.uint8,))
+        _arg(scales, "scales", self._ng, (torch.float32,))
+        _arg(hard_loss, "hard_loss", self.cfg.batch, (torch.float32,))
         _check(load().gsq_harden(self.handle, _ptr(codes), _ptr(scales), _ptr(hard_loss),
                                  _stream(stream)))
 
     def pack(self, out, stream=None):
+        if not (out.is_cuda and out.is_contiguous()):
+            raise ValueError("out must be a contiguous device tensor")
         _check(load().gsq_pack(self.handle, _ptr(out), out.numel() * out.element_size(),
                                _stream(stream)))
 
     def get_state(self, logits=None, m=None, v=None, scales=None, m_s=None, v_s=None, base=None,
                   stream=None):
+        self._state_args(logits, m, v, scales, m_s, v_s, base)
         t = ctypes.c_int64()
         _check(load().gsq_get_state(self.handle, _ptr(logits), _ptr(m), _ptr(v), _ptr(scales),
                                     _ptr(m_s), _ptr(v_s), _ptr(base), ctypes.byref(t),
@@ -224,10 +265,23 @@ class Layer:
 
     def set_state(self, t, logits=None, m=None, v=None, scales=None, m_s=None, v_s=None, base=None,
                   stream=None):
+        self._state_args(logits, m, v, scales, m_s, v_s, base)
         _check(load().gsq_set_state(self.handle, _ptr(logits), _ptr(m), _ptr(v), _ptr(scales),
                                     _ptr(m_s), _ptr(v_s), _ptr(base), int(t), _stream(stream)))
 
+    def _state_args(self, logits, m, v, scales, m_s, v_s, base):
+        import torch
+        for name, x in (("logits", logits), ("m", m), ("v", v)):
+            _arg(x, name, self._n * self.cfg.K, (torch.float32,))
+        for name, x in (("scales", scales), ("m_s", m_s), ("v_s", v_s)):
+            _arg(x, name, self._ng, (torch.float32,))
+        _arg(base, "base", self._n, (torch.uint8,))
+
     def intermediates(self, residual=None, grad=None, stream=None):
+        import torch
+        _arg(residual, "residual", self._n,
+             (torch.bfloat16,) if self.cfg.precision == PREC_BF16 else (torch.float32,))
+        _arg(grad, "grad", self._n, (torch.float32,))
         _check(load().gsq_get_intermediates(self.handle, _ptr(residual), _ptr(grad), _stream(stream)))
 
     def timing(self, enable):

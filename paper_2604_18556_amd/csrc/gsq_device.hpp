@@ -60,32 +60,55 @@ __device__ __forceinline__ float gumbel_fast(uint32_t x) {
   return __builtin_amdgcn_logf(nl) * -kLn2;
 }
 
-template <bool kExact>
-__device__ __forceinline__ float gumbel(uint32_t x) {
-  if constexpr (kExact) return gumbel_exact(x); else return gumbel_fast(x);
+// Logistic(0,1) sample ln u - ln(1 - u), the noise of a two-value relaxation with logits
+// {-l, l}: its softmax sees the two Gumbel values only through their difference, which has this
+// law.  1 - u is exact in fp32 (u has at most 24 significant bits below 1).  Exact: evaluated in
+// fp64 and rounded once to fp32; fast: ln2 (log2 u - log2(1 - u)) with the hardware logarithm.
+__device__ __forceinline__ float logistic_exact(uint32_t x) {
+  const float u = uniform01(x);
+  return (float)(log((double)u) - log((double)(1.0f - u)));
 }
 
-// The 4 x K Gumbel values of the chunk starting at e0 (a multiple of 4) at step t.
-template <int K, bool kExact>
+__device__ __forceinline__ float logistic_fast(uint32_t x) {
+  constexpr float kLn2 = 0.69314718055994531f;
+  const float u = uniform01(x);
+  return (__builtin_amdgcn_logf(u) - __builtin_amdgcn_logf(1.0f - u)) * kLn2;
+}
+
+// Transform of a noise word: Gumbel values for categoricals, logistic values for binary pairs.
+enum NoiseKind { kGumbel = 0, kLogistic = 1 };
+
+template <int kKind, bool kExact>
+__device__ __forceinline__ float noise_value(uint32_t x) {
+  if constexpr (kKind == kLogistic) {
+    if constexpr (kExact) return logistic_exact(x); else return logistic_fast(x);
+  } else {
+    if constexpr (kExact) return gumbel_exact(x); else return gumbel_fast(x);
+  }
+}
+
+// The 4 x K noise values of the chunk starting at e0 (a multiple of 4) at step t.
+template <int K, bool kExact, int kKind = kGumbel>
 __device__ __forceinline__ void draw_chunk(float (&g)[4][K], uint64_t seed, uint64_t e0, uint32_t t,
                                            uint32_t sample) {
 #pragma unroll
   for (int j = 0; j < K; ++j) {
     const U4 w = noise_words(seed, e0, t, sample * 256u, (uint32_t)j);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) g[(4 * j + r) / K][(4 * j + r) % K] = gumbel<kExact>(word_of(w, r));
+    for (int r = 0; r < 4; ++r)
+      g[(4 * j + r) / K][(4 * j + r) % K] = noise_value<kKind, kExact>(word_of(w, r));
   }
 }
 
-// The K Gumbel values of one coordinate e at step t (any e; draws only the calls it needs).
-template <int K, bool kExact>
+// The K noise values of one coordinate e at step t (any e; draws only the calls it needs).
+template <int K, bool kExact, int kKind = kGumbel>
 __device__ __forceinline__ void draw_one(float (&g)[K], uint64_t seed, uint64_t e, uint32_t t) {
   const uint64_t e0 = e & ~(uint64_t)3;
   const int q = (int)(e & 3);
 #pragma unroll
   for (int k = 0; k < K; ++k) {
     const int f = q * K + k;
-    g[k] = gumbel<kExact>(word_of(noise_words(seed, e0, t, 0u, (uint32_t)(f >> 2)), f & 3));
+    g[k] = noise_value<kKind, kExact>(word_of(noise_words(seed, e0, t, 0u, (uint32_t)(f >> 2)), f & 3));
   }
 }
 

@@ -143,13 +143,14 @@ __device__ __forceinline__ void soft_sample(const float (&l)[K], const float (&c
 }
 
 // Two-value relaxation with logits {-l, l} (§3): p1 = softmax over (-kappa l + g0,
-// kappa l + g1) / tau, i.e. a sigmoid of (2 kappa l + g1 - g0) / tau.  The smaller
-// probability is formed as e / (1 + e) with e = exp(-|a|), never as 1 - p.
+// kappa l + g1) / tau, i.e. a sigmoid of (2 kappa l + g1 - g0) / tau.  The pair's noise dn is
+// drawn as the difference g1 - g0 itself (a logistic value).  The smaller probability is formed
+// as e / (1 + e) with e = exp(-|a|), never as 1 - p.
 template <bool kF64>
-__device__ __forceinline__ void pair_probs(float l, float g0, float g1, float kappa, Real<kF64> inv_tau,
+__device__ __forceinline__ void pair_probs(float l, float dn, float kappa, Real<kF64> inv_tau,
                                            Real<kF64>& p0, Real<kF64>& p1) {
   using T = Real<kF64>;
-  const T d = (T)2 * (T)kappa * (T)l + ((T)g1 - (T)g0);
+  const T d = (T)2 * (T)kappa * (T)l + (T)dn;
   const T a = d * inv_tau;
   T e, big;
   if constexpr (kF64) {
@@ -164,9 +165,13 @@ __device__ __forceinline__ void pair_probs(float l, float g0, float g1, float ka
   p0 = a >= T(0) ? small : big;
 }
 
-// Gumbel values per coordinate and draw: one per logit, or the mask's two and the sign's two.
+// Noise values per coordinate and draw: one Gumbel value per logit of a categorical, or one
+// logistic value per binary pair (the mask's, then the sign's).
 template <int K, int kMode>
-constexpr int noise_count() { return kMode == GSQ_RELAX_TERNARY ? 4 : K; }
+constexpr int noise_count() { return kMode == GSQ_RELAX_TERNARY ? 2 : K; }
+
+template <int kMode>
+constexpr int noise_kind() { return kMode == GSQ_RELAX_TERNARY ? kLogistic : kGumbel; }
 
 // One coordinate's relaxed sample in any relaxation: the soft level v (W_hat = s v) and
 // jac[k] = (tau / kappa) dv/dl_k.
@@ -180,10 +185,10 @@ __device__ __forceinline__ void coord_sample(const float (&l)[K], const float (&
                                              Real<kF64> (&jac)[K]) {
   using T = Real<kF64>;
   if constexpr (kMode == GSQ_RELAX_TERNARY) {
-    static_assert(K == 2 && Z == 4, "ternary: two logits, four noise values");
+    static_assert(K == 2 && Z == 2, "ternary: two logits, one noise value per pair");
     T pm0, pm1, pb0, pb1;
-    pair_probs<kF64>(l[0], g[0], g[1], kappa, inv_tau, pm0, pm1);
-    pair_probs<kF64>(l[1], g[2], g[3], kappa, inv_tau, pb0, pb1);
+    pair_probs<kF64>(l[0], g[0], kappa, inv_tau, pm0, pm1);
+    pair_probs<kF64>(l[1], g[1], kappa, inv_tau, pb0, pb1);
     const T m = pm1, b = pb1 - pb0;
     v = m * b;
     jac[0] = b * (T(2) * pm0 * pm1);
@@ -243,11 +248,11 @@ __device__ __forceinline__ void coord_candidates(float (&cand)[K], const ElemArg
 }
 
 // Noise of the thread's chunk of four coordinates (or zeros when sampling is off).
-template <int Z, bool kF64>
+template <int Z, bool kF64, int kMode>
 __device__ __forceinline__ void chunk_noise(float (&g)[4][Z], const ElemArgs& a, uint64_t e0,
                                             uint32_t t, uint32_t sample) {
   if (a.noise) {
-    draw_chunk<Z, kF64>(g, a.seed, e0, t, sample);
+    draw_chunk<Z, kF64, noise_kind<kMode>()>(g, a.seed, e0, t, sample);
   } else {
 #pragma unroll
     for (int q = 0; q < 4; ++q)
@@ -279,7 +284,7 @@ __global__ __launch_bounds__(kBlock) void k_forward(ElemArgs a) {
     for (int k = 0; k < K; ++k) lv[k] = *reinterpret_cast<const float4*>(a.L + state_off(e0, k, K));
     const uint32_t j4 = chunk_bases<kMode>(a, e0);
     float g[4][Z];
-    chunk_noise<Z, kF64>(g, a, (uint64_t)e0, a.t, (uint32_t)a.sample);
+    chunk_noise<Z, kF64, kMode>(g, a, (uint64_t)e0, a.t, (uint32_t)a.sample);
     float r[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -418,7 +423,7 @@ __global__ __launch_bounds__(kBlock) void k_backward(
       const float4 gv = active ? ld_stream(a.G + smp * a.g_stride + gidx)
                                : make_float4(0.f, 0.f, 0.f, 0.f);
       float g[4][Z];
-      chunk_noise<Z, kF64>(g, a, (uint64_t)e0, a.t, (uint32_t)smp);
+      chunk_noise<Z, kF64, kMode>(g, a, (uint64_t)e0, a.t, (uint32_t)smp);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         float l[K], cand[K];
@@ -471,7 +476,9 @@ __global__ __launch_bounds__(kBlock) void k_backward(
           f4set(lv[k], q, (float)th);
         }
         if (active) {
-          bad |= !(finite4(lv[k]) && finite4(vk));
+          // a non-finite gradient reaches v under Adam, and m under Lion (whose step is only
+          // a sign and stays finite)
+          bad |= !(finite4(lv[k]) && finite4(lion ? mk : vk));
           const int64_t o = state_off(e0, k, K);
           st_stream(a.L + o, lv[k]);
           st_stream(a.M + o, mk);
@@ -501,7 +508,7 @@ __global__ __launch_bounds__(kBlock) void k_backward(
       if (active) {
 #pragma unroll
         for (int k = 0; k < K; ++k) {
-          bad |= !(finite4(lv[k]) && finite4(vv[k]));
+          bad |= !(finite4(lv[k]) && finite4(lion ? mv[k] : vv[k]));
           const int64_t o = state_off(e0, k, K);
           st_stream(a.L + o, lv[k]);
           st_stream(a.M + o, mv[k]);
@@ -520,7 +527,7 @@ __global__ __launch_bounds__(kBlock) void k_backward(
         opt_update<kF64, kLion>(ds_part, th, m1, v1, (T)a.lr_s, step_s, b1, b2, omb1, omb2, rbc2,
                          eps, wd);
         s_new = (float)th;
-        bad |= !(__builtin_isfinite(s_new) && __builtin_isfinite((float)v1));
+        bad |= !(__builtin_isfinite(s_new) && __builtin_isfinite((float)(lion ? m1 : v1)));
         a.MS[sidx] = (float)m1;
         a.VS[sidx] = (float)v1;
         a.S[sidx] = s_new;
@@ -530,7 +537,7 @@ __global__ __launch_bounds__(kBlock) void k_backward(
     if (a.fuse && active) {
       const T inv_tau_n = kF64 ? (T)a.inv_tau_n_d : (T)a.inv_tau_n;
       float g[4][Z];
-      chunk_noise<Z, kF64>(g, a, (uint64_t)e0, a.t_next, 0u);
+      chunk_noise<Z, kF64, kMode>(g, a, (uint64_t)e0, a.t_next, 0u);
       float r[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
@@ -807,26 +814,63 @@ __global__ void k_pack_scales(const float* S, uint8_t* out, int64_t n, int* flag
 }
 
 // Super-block layout: one 110-byte record per 256 weights,
-// [fp16 d][16 x 6-bit sc, LSB first][256 x 3-bit codes, LSB first].
-__global__ void k_pack_superblock(const uint8_t* codes, const uint16_t* D, const uint8_t* SC,
-                                  uint8_t* out, int64_t nrec) {
-  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < nrec;
-       r += (int64_t)gridDim.x * blockDim.x) {
-    uint8_t* o = out + r * 110;
-    o[0] = (uint8_t)D[r];
-    o[1] = (uint8_t)(D[r] >> 8);
-    uint64_t acc = 0;
-    int nbits = 0, pos = 2;
-    for (int j = 0; j < 16; ++j) {
-      acc |= (uint64_t)(SC[r * 16 + j] & 63u) << nbits;
-      nbits += 6;
-      while (nbits >= 8) { o[pos++] = (uint8_t)acc; acc >>= 8; nbits -= 8; }
+// [fp16 d][16 x 6-bit sc, LSB first][256 x 3-bit codes, LSB first].  A block builds kSbRecs
+// consecutive records in LDS (the 3-bit codes of 16 weights fill 6 whole bytes, the 16 sub-block
+// scales 12) and writes them out as one contiguous run, so that the code reads (16 bytes per
+// lane) and the record writes (4 bytes per lane where `out` allows) are both coalesced.
+constexpr int kSbRecs = 64;
+constexpr int kSbBytes = 110;
+
+__global__ __launch_bounds__(256) void k_pack_superblock(const uint8_t* __restrict__ codes,
+                                                         const uint16_t* __restrict__ D,
+                                                         const uint8_t* __restrict__ SC,
+                                                         uint8_t* __restrict__ out, int64_t nrec) {
+  __shared__ __align__(16) uint8_t buf[kSbRecs * kSbBytes];
+  const bool words = (reinterpret_cast<uintptr_t>(out) & 3) == 0;
+  for (int64_t r0 = (int64_t)blockIdx.x * kSbRecs; r0 < nrec; r0 += (int64_t)gridDim.x * kSbRecs) {
+    const int nr = (int)(nrec - r0 < kSbRecs ? nrec - r0 : kSbRecs);
+    // codes: piece p = codes 16 p .. 16 p + 15 of the run -> 6 bytes of record p / 16
+    const uint8_t* src = codes + r0 * 256;
+    for (int p = threadIdx.x; p < nr * 16; p += blockDim.x) {
+      const uint4 c = *reinterpret_cast<const uint4*>(src + 16 * (int64_t)p);
+      const uint32_t w4[4] = {c.x, c.y, c.z, c.w};
+      uint64_t bits = 0;
+#pragma unroll
+      for (int q = 0; q < 16; ++q) bits |= (uint64_t)((w4[q >> 2] >> (8 * (q & 3))) & 7u) << (3 * q);
+      uint8_t* o = buf + (p >> 4) * kSbBytes + 14 + 6 * (p & 15);
+#pragma unroll
+      for (int b = 0; b < 6; ++b) o[b] = (uint8_t)(bits >> (8 * b));
     }
-    for (int i = 0; i < 256; ++i) {
-      acc |= (uint64_t)(codes[r * 256 + i] & 7u) << nbits;
-      nbits += 3;
-      while (nbits >= 8) { o[pos++] = (uint8_t)acc; acc >>= 8; nbits -= 8; }
+    // header of each record: d, then the 96 bits of the 16 sub-block scales
+    for (int rec = threadIdx.x; rec < nr; rec += blockDim.x) {
+      const int64_t r = r0 + rec;
+      uint8_t* o = buf + rec * kSbBytes;
+      const uint16_t d = D[r];
+      o[0] = (uint8_t)d;
+      o[1] = (uint8_t)(d >> 8);
+      const uint4 sc = *reinterpret_cast<const uint4*>(SC + 16 * r);
+      const uint32_t s4[4] = {sc.x, sc.y, sc.z, sc.w};
+      uint64_t lo = 0, hi = 0;   // bits 0..63 and 64..95 of the scale field
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const uint64_t v = (s4[j >> 2] >> (8 * (j & 3))) & 63u;
+        const int at = 6 * j;
+        if (at < 64) lo |= v << at;
+        if (at + 6 > 64) hi |= at >= 64 ? v << (at - 64) : v >> (64 - at);
+      }
+#pragma unroll
+      for (int b = 0; b < 8; ++b) o[2 + b] = (uint8_t)(lo >> (8 * b));
+#pragma unroll
+      for (int b = 0; b < 4; ++b) o[10 + b] = (uint8_t)(hi >> (8 * b));
     }
+    __syncthreads();
+    uint8_t* dst = out + r0 * kSbBytes;   // r0 kSbBytes is a multiple of 4
+    const int nbytes = nr * kSbBytes;
+    const int nw = words ? nbytes / 4 : 0;
+    for (int i = threadIdx.x; i < nw; i += blockDim.x)
+      reinterpret_cast<uint32_t*>(dst)[i] = reinterpret_cast<const uint32_t*>(buf)[i];
+    for (int i = 4 * nw + threadIdx.x; i < nbytes; i += blockDim.x) dst[i] = buf[i];
+    __syncthreads();   // buf is refilled by the next run
   }
 }
 
@@ -856,12 +900,12 @@ __global__ void k_unpad(const uint8_t* src, uint8_t* dst, int64_t N, int64_t O, 
 }
 
 // ------------------------------------------------------------------ noise probe
-template <int K, bool kExact>
+template <int K, bool kExact, int kKind>
 __global__ void k_gumbel(uint64_t seed, int64_t e0, int64_t count, uint32_t t, float* out) {
   for (int64_t n = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; n < count;
        n += (int64_t)gridDim.x * blockDim.x) {
     float g[K];
-    draw_one<K, kExact>(g, seed, (uint64_t)(e0 + n), t);
+    draw_one<K, kExact, kKind>(g, seed, (uint64_t)(e0 + n), t);
     for (int k = 0; k < K; ++k) out[n * K + k] = g[k];
   }
 }
@@ -1037,8 +1081,8 @@ hipError_t launch_eff_scales(const Layer& L, float* out, hipStream_t s) {
 hipError_t launch_pack(const Layer& L, const uint8_t* codes, uint8_t* out, hipStream_t s) {
   if (L.cfg.layout == GSQ_LAYOUT_SUPERBLOCK) {
     const int64_t nrec = L.N / 256;
-    hipLaunchKernelGGL(k_pack_superblock, flat_grid(nrec), dim3(256), 0, s, codes, L.sb_d, L.sb_sc,
-                       out, nrec);
+    hipLaunchKernelGGL(k_pack_superblock, flat_grid((nrec + kSbRecs - 1) / kSbRecs, 1), dim3(256), 0,
+                       s, codes, L.sb_d, L.sb_sc, out, nrec);
     return hipGetLastError();
   }
   int64_t code_bytes;
@@ -1079,22 +1123,22 @@ hipError_t launch_copy_grad(const Layer& L, const float* Gpad, float* out, hipSt
   return hipGetLastError();
 }
 
-template <int K>
+template <int K, int kKind = kGumbel>
 static hipError_t gumbel_k(const gsq_config& cfg, int64_t e0, int64_t count, int64_t t, float* out,
                            hipStream_t s) {
   if (cfg.precision == GSQ_PREC_BF16)
-    hipLaunchKernelGGL((k_gumbel<K, false>), flat_grid(count), dim3(256), 0, s, cfg.seed, e0, count,
-                       (uint32_t)t, out);
+    hipLaunchKernelGGL((k_gumbel<K, false, kKind>), flat_grid(count), dim3(256), 0, s, cfg.seed, e0,
+                       count, (uint32_t)t, out);
   else
-    hipLaunchKernelGGL((k_gumbel<K, true>), flat_grid(count), dim3(256), 0, s, cfg.seed, e0, count,
-                       (uint32_t)t, out);
+    hipLaunchKernelGGL((k_gumbel<K, true, kKind>), flat_grid(count), dim3(256), 0, s, cfg.seed, e0,
+                       count, (uint32_t)t, out);
   return hipGetLastError();
 }
 
 hipError_t launch_gumbel(const gsq_config& cfg, int64_t e0, int64_t count, int64_t t, float* out,
                          hipStream_t s) {
-  const int z = cfg.relaxation == GSQ_RELAX_SHIFT ? GSQ_SHIFT_WINDOW
-                : cfg.relaxation == GSQ_RELAX_TERNARY ? 4 : cfg.n_levels;
+  if (cfg.relaxation == GSQ_RELAX_TERNARY) return gumbel_k<2, kLogistic>(cfg, e0, count, t, out, s);
+  const int z = cfg.relaxation == GSQ_RELAX_SHIFT ? GSQ_SHIFT_WINDOW : cfg.n_levels;
   switch (z) {
     case 2: return gumbel_k<2>(cfg, e0, count, t, out, s);
     case 3: return gumbel_k<3>(cfg, e0, count, t, out, s);

@@ -116,6 +116,10 @@ CASES = [
     ("bf16", 1, 40, 384, 7, 128, "group", 0.1, 1.0),
     ("fp32", 1, 24, 256, 6, 64, "group", 0.3, 1.0),
     ("fp32", 1, 24, 256, 8, 128, "group", 0.3, 1.0),
+    # more than one chunk (2048 row partials) of the loss reduction per layer: 2304 and
+    # 3 x 2000 partials, so the fixed-order chunk sums and the last-block hand-off are exercised
+    ("fp32", 1, 2304, 256, 4, 128, "group", 0.3, 1.0),
+    ("bf16", 2, 3000, 512, 4, 128, "group", 0.3, 1.0),
 ]
 
 
@@ -437,22 +441,49 @@ def _full_size_steps(dev, name, extra, blas):
                            dlogits=inter["dlogits"])
         lv = loss.cpu().numpy()
         assert np.all(np.isfinite(lv)) and np.all(lv > 0)
+        if extra.get("samples", 1) == 1:
+            # the step loss of every layer against sum(R (-G / 2)) over the whole layer, summed
+            # in fp64 by torch from the layer's own R and G: the whole multi-chunk reduction of
+            # the backward's row partials at the real shape
+            R = torch.empty(Bn, O, I, dtype=torch.bfloat16, device=dev)
+            G = torch.empty(Bn, O, I, device=dev)
+            layer.intermediates(residual=R, grad=G)
+            for e in range(Bn):
+                want = float((R[e].double() * G[e].double()).sum() * -0.5)
+                assert abs(lv[e] - want) <= 1e-4 * abs(want), (name, t, e, lv[e], want)
+            del R, G
         st = st_new
     if blas:
-        _check_full_size_harden_and_pack(dev, layer, w, pair_cfg, rcfg, st, gst, experts, rows)
+        _check_full_size_harden_and_pack(dev, layer, w, pair_cfg, rcfg, st, gst, experts, rows, W,
+                                         Hs_bf)
     layer.destroy()
 
 
-def _check_full_size_harden_and_pack(dev, layer, w, pair_cfg, rcfg, st, gst, experts, rows):
+def _check_full_size_harden_and_pack(dev, layer, w, pair_cfg, rcfg, st, gst, experts, rows, W,
+                                     Hs_bf):
     """gsq_harden and gsq_pack on the whole layer: the codes of the sampled rows are the
     oracle's hardening of the layer's own logits for those rows, and those rows' bytes in the
-    packed output are the oracle packer's (64-bit offsets: the MoE stream spans 2.8e9 bits)."""
+    packed output are the oracle packer's (64-bit offsets: the MoE stream spans 2.8e9 bits).
+    The hard loss of each sampled expert equals tr(R_h H R_h^T), R_h = W - s c[q] built by
+    torch from the returned codes and effective scales, H the library's bf16 H, products by the
+    vendor BLAS: the contraction's tile partials through the multi-chunk reduction."""
     Bn, O, I, n = w.batch, w.out_features, w.in_features, len(w.levels)
     gst.base = st.base
     c_ref = ref.hard_codes(rcfg, gst)
     codes = torch.empty(Bn, O, I, dtype=torch.uint8, device=dev)
-    layer.harden(codes=codes)
+    eff = torch.empty(Bn, O, I // pair_cfg.gs, device=dev)
+    hl = torch.empty(Bn, device=dev)
+    layer.harden(codes=codes, scales=eff, hard_loss=hl)
     c_gpu = np.stack([codes[e].cpu().numpy()[rows] for e in experts])
+    lev = torch.tensor(w.levels, dtype=torch.float32, device=dev)
+    for e in experts:
+        Wq = eff[e].repeat_interleave(pair_cfg.gs, dim=-1) * lev[codes[e].long()]
+        Rh = (torch.from_numpy(W[e]).to(dev) - Wq).to(torch.bfloat16)
+        P = torch.mm(Rh, Hs_bf[e], out_dtype=torch.float32)
+        want = float((Rh.double() * P.double()).sum())
+        got = float(hl[e])
+        assert abs(got - want) <= 1e-3 * abs(want), (w.name, e, got, want)
+        del Wq, Rh, P
     del codes
     np.testing.assert_array_equal(c_gpu, c_ref)
     packed = torch.empty(B.packed_size(pair_cfg), dtype=torch.uint8, device=dev)

@@ -37,15 +37,31 @@ def _rcfg(relax, O, I, levels, gs, prec, **kw):
 
 
 # ------------------------------------------------------------------ noise
-@pytest.mark.parametrize("relax,levels,Z", [("shift", L8, 5), ("ternary", L3, 4)])
+@pytest.mark.parametrize("relax,levels,Z", [("shift", L8, 5), ("ternary", L3, 2)])
 def test_noise_of_the_relaxations_is_bit_exact(dev, relax, levels, Z):
+    """FP32 precision: Gumbel values of the shift's five logits, logistic values of the ternary
+    relaxation's two pairs, both evaluated in fp64 and rounded once, as the oracle does."""
     cfg = B.LayerConfig(4, 256, levels, 128, precision=B.PREC_FP32, seed=77,
                         relaxation={"shift": B.RELAX_SHIFT, "ternary": B.RELAX_TERNARY}[relax])
     n = 100_000
     out = torch.empty(n, Z, device=dev)
     B.gumbel(cfg, 3 * 2**32 - 17, n, 5, out)
-    want = philox.gumbel(77, np.arange(3 * 2**32 - 17, 3 * 2**32 - 17 + n), 5, Z)
+    draw = philox.logistic if relax == "ternary" else philox.gumbel
+    want = draw(77, np.arange(3 * 2**32 - 17, 3 * 2**32 - 17 + n), 5, Z)
     assert np.count_nonzero(out.cpu().numpy().astype(np.float64) != want) <= 2
+
+
+def test_ternary_noise_bf16_path_is_close(dev):
+    """BF16 precision: ln2 (log2 u - log2(1 - u)) with the hardware logarithm against the fp64
+    value; the error is a few ulps of the larger logarithm."""
+    cfg = B.LayerConfig(4, 256, L3, 128, precision=B.PREC_BF16, seed=5, relaxation=B.RELAX_TERNARY)
+    n = 400_000
+    out = torch.empty(n, 2, device=dev)
+    B.gumbel(cfg, 0, n, 3, out)
+    want = philox.logistic(5, np.arange(n), 3, 2)
+    err = np.abs(out.cpu().numpy() - want)
+    print(f"bf16-path logistic noise: max abs error {err.max():.3e}, mean {err.mean():.3e}")
+    assert err.max() < 2e-5, err.max()
 
 
 # ------------------------------------------------------------------ initialisation
