@@ -317,6 +317,23 @@ def test_non_finite_weights_are_reported(dev):
     assert e.value.status == B.GSQ_EINVAL
 
 
+@pytest.mark.parametrize("opt", ["lion", "adam"])
+def test_non_finite_gradients_are_reported_without_a_loss(dev, opt):
+    """A NaN in H makes a column of G NaN.  Lion's step is a sign, so the logits and scales stay
+    finite and only the moments carry the NaN; the flag must still be set when the steps
+    request no loss (nothing else would read the gradient)."""
+    W, H = layer_inputs(32, 256, seed=3)
+    H[0, 7, 7] = np.nan
+    rcfg = ref.Config(32, 256, L4, 128, precision="bf16")
+    pair = Pair(rcfg, W, H, dev)
+    kw = dict(optimizer=B.OPT_LION, lr_logits=1e-4, weight_decay=1.0) if opt == "lion" else {}
+    for t in range(2):
+        pair.layer.step(B.StepParams(tau=0.5, lr_scales=5e-5, **kw), loss_out=None)
+    with pytest.raises(B.GsqError) as e:
+        pair.layer.check()
+    assert e.value.status == B.GSQ_ENONFINITE
+
+
 def test_superblock_rejects_scale_training(dev):
     W, H = layer_inputs(16, 256, seed=2)
     rcfg = ref.Config(16, 256, L8, layout="superblock", precision="bf16")
