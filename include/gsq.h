@@ -153,6 +153,23 @@ gsq_status gsq_layer_init(const gsq_config* cfg, const void* W, int32_t w_dtype,
 gsq_status gsq_step(gsq_layer* h, const gsq_step_params* p, float* loss_out, hipStream_t stream);
 
 /*
+ * gsq_step for callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc).  The same step, with the same results bit for
+ * bit, but it allocates nothing: the scratch of the loss reduction (row partials, chunk sums, one
+ * ticket per layer) lives in a static device array of the library, about 33 MiB per GPU, held
+ * until the process ends, instead of in the handle's buffers; and the per-sample gradient
+ * buffers are never grown.
+ * Limits (GSQ_EINVAL before anything is enqueued): samples at most the most any earlier gsq_step
+ * on this handle used (1 for a new handle); with loss_out, batch * O * ceil(I / 256) <= 4194304
+ * row partials, batch * ceil(O * ceil(I / 256) / 2048) <= 65536 chunk sums and batch <= 65536.
+ * The handle's device must be current.  Every call on one GPU shares that GPU's scratch, which
+ * keeps the last call's contents: calls that overlap on one GPU (other streams, threads or
+ * handles) race, and the caller must order them.
+ */
+gsq_status gsq_step_static(gsq_layer* h, const gsq_step_params* p, float* loss_out,
+                           hipStream_t stream);
+
+/*
  * Harden (the final step of Alg. 2): codes into `codes` (device u8, batch x O x I, or NULL),
  * code = grid level index.  GRID: argmax_k logits (ties to the lowest k); SHIFT:
  * clip(j0 + delta*) with delta* the argmax shift (ties to the lowest); TERNARY: mask

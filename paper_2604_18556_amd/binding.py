@@ -22,8 +22,8 @@ MAX_SAMPLES = 16            # GSQ_MAX_SAMPLES
 STATUS_NAMES = {0: "GSQ_OK", -1: "GSQ_EINVAL", -2: "GSQ_ENOMEM", -3: "GSQ_EHIP",
                 -4: "GSQ_ENONFINITE", -5: "GSQ_EUNSUPPORTED"}
 
-EXPORTS = ("gsq_layer_init", "gsq_step", "gsq_harden", "gsq_packed_size", "gsq_pack",
-           "gsq_get_state", "gsq_set_state", "gsq_get_intermediates", "gsq_gumbel", "gsq_check",
+EXPORTS = ("gsq_layer_init", "gsq_step", "gsq_step_static", "gsq_harden", "gsq_packed_size",
+           "gsq_pack", "gsq_get_state", "gsq_set_state", "gsq_get_intermediates", "gsq_gumbel", "gsq_check",
            "gsq_layer_destroy", "gsq_last_error", "gsq_timing", "gsq_timing_read")
 KERNEL_NAMES = ("init", "forward", "contract", "reduce", "backward", "harden", "pack")
 
@@ -127,6 +127,7 @@ def load(path=None):
     vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     lib.gsq_layer_init.argtypes = [ctypes.POINTER(CConfig), vp, i32, vp, vp, vp, ctypes.POINTER(vp)]
     lib.gsq_step.argtypes = [vp, ctypes.POINTER(CStepParams), vp, vp]
+    lib.gsq_step_static.argtypes = [vp, ctypes.POINTER(CStepParams), vp, vp]
     lib.gsq_harden.argtypes = [vp, vp, vp, vp, vp]
     lib.gsq_packed_size.argtypes = [ctypes.POINTER(CConfig)]
     lib.gsq_packed_size.restype = sz
@@ -140,8 +141,8 @@ def load(path=None):
     lib.gsq_last_error.restype = ctypes.c_char_p
     lib.gsq_timing.argtypes = [vp, i32]
     lib.gsq_timing_read.argtypes = [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64), i32, vp]
-    for name in ("gsq_layer_init", "gsq_step", "gsq_harden", "gsq_pack", "gsq_get_state",
-                 "gsq_set_state", "gsq_get_intermediates", "gsq_gumbel", "gsq_check",
+    for name in ("gsq_layer_init", "gsq_step", "gsq_step_static", "gsq_harden", "gsq_pack",
+                 "gsq_get_state", "gsq_set_state", "gsq_get_intermediates", "gsq_gumbel", "gsq_check",
                  "gsq_layer_destroy", "gsq_timing", "gsq_timing_read"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
@@ -239,6 +240,13 @@ class Layer:
         _arg(loss_out, "loss_out", self.cfg.batch, (torch.float32,))
         _check(load().gsq_step(self.handle, ctypes.byref(params.to_c()), _ptr(loss_out),
                                _stream(stream)))
+
+    def step_static(self, params, loss_out=None, stream=None):
+        """gsq_step_static: the same step with no allocation (static scratch of the library)."""
+        import torch
+        _arg(loss_out, "loss_out", self.cfg.batch, (torch.float32,))
+        _check(load().gsq_step_static(self.handle, ctypes.byref(params.to_c()), _ptr(loss_out),
+                                      _stream(stream)))
 
     def harden(self, codes=None, scales=None, hard_loss=None, stream=None):
         import torch

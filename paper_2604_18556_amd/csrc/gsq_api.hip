@@ -5,6 +5,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 
@@ -171,6 +172,41 @@ gsq_status check_flag(gsq::Layer* h, hipStream_t s) {
   return GSQ_OK;
 }
 
+// ---- scratch of gsq_step_static: a file-scope device array instead of the handle's buffers.
+// It holds the loss reduction's row partials, chunk sums and per-layer tickets.  Each GPU holds
+// its own copy until the process ends; host code reaches it only through the address
+// hipGetSymbolAddress returns for the current device (taken once per device, at the first
+// gsq_layer_init on it).  Every gsq_step_static call on a GPU shares that GPU's copy.
+constexpr size_t kStaticPartials = (size_t)4 << 20;   // row partials (fp64): 32 MiB
+constexpr size_t kStaticStage = (size_t)1 << 16;      // chunk sums (fp64): 512 KiB
+constexpr size_t kStaticTickets = (size_t)1 << 16;    // one per layer (u32): 256 KiB
+constexpr size_t kStaticBytes = (kStaticPartials + kStaticStage) * 8 + kStaticTickets * 4;
+static __device__ __align__(256) unsigned char scratch[kStaticBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {nullptr};
+
+// Address of this device's scratch (device `dev` current), set up on first use: the ticket
+// region is cleared, since the reduction leaves tickets at zero but needs them zero on entry.
+// Synchronises `stream` the first time only.
+hipError_t static_scratch(int dev, hipStream_t stream, void** out) {
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    unsigned char* base = static_cast<unsigned char*>(ptr);
+    e = hipMemsetAsync(base + (kStaticPartials + kStaticStage) * 8, 0, kStaticTickets * 4, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
 }  // namespace
 
 struct gsq_layer : gsq::Layer {};
@@ -221,9 +257,11 @@ gsq_status gsq_layer_init(const gsq_config* cfg, const void* W, int32_t w_dtype,
   L.loss_cols = (L.I + 255) / 256;
   {
     int dev = 0, ncu = 0;
-    if (hipGetDevice(&dev) == hipSuccess &&
-        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess)
-      gsq::plan_contract_split(L, ncu);
+    if (hipGetDevice(&dev) == hipSuccess) {
+      L.device = dev;
+      if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess)
+        gsq::plan_contract_split(L, ncu);
+    }
     (void)hipGetLastError();
   }
   if (L.bf16) {
@@ -280,6 +318,12 @@ gsq_status gsq_layer_init(const gsq_config* cfg, const void* W, int32_t w_dtype,
     free_layer(h);
     return st;
   }
+  {
+    // gsq_step_static's scratch on this device (once per device); a failure here only disables
+    // that entry point, which then reports it
+    void* unused = nullptr;
+    if (static_scratch(L.device, stream, &unused) != hipSuccess) (void)hipGetLastError();
+  }
   *out = h;
   return GSQ_OK;
 }
@@ -325,20 +369,19 @@ static gsq_status validate_params(const gsq_layer* h, const gsq_step_params* p) 
   return GSQ_OK;
 }
 
-gsq_status gsq_step(gsq_layer* h, const gsq_step_params* p, float* loss_out, hipStream_t stream) {
-  g_err.clear();
-  if (!h) return fail(GSQ_EINVAL, "handle is NULL");
-  gsq_status st = validate_params(h, p);
-  if (st != GSQ_OK) return st;
-  gsq::Layer& L = *h;
-  if (L.t >= (int64_t)UINT32_MAX) return fail(GSQ_EINVAL, "step counter exhausted");
-  // grow the per-sample buffers before any launch argument captures their addresses
+// Buffers of the loss reduction of one step: the handle's own, or gsq_step_static's scratch.
+struct LossBuffers {
+  double* part;
+  double* stage;
+  unsigned* tickets;
+};
+
+// The body of gsq_step and gsq_step_static, after validation (M sample slots exist).
+static gsq_status step_impl(gsq::Layer& L, const gsq_step_params* p, float* loss_out,
+                            const LossBuffers& lb, hipStream_t stream) {
   const int M = p->samples > 1 ? p->samples : 1;
-  if (M > L.sample_slots) {
-    gsq_status st2 = grow_sample_slots(L, M);
-    if (st2 != GSQ_OK) return st2;
-  }
   gsq::ElemArgs a = gsq::base_args(L);
+  a.loss_part = lb.part;
   a.t = (uint32_t)L.t;
   a.noise = p->gumbel_noise ? 1 : 0;
   a.kappa = p->kappa;
@@ -386,7 +429,10 @@ gsq_status gsq_step(gsq_layer* h, const gsq_step_params* p, float* loss_out, hip
   a.inv_tau_n_d = a.fuse ? 1.0 / (double)p->tau_next : 0.0;
   a.Rout = L.R[1 - use];
   GSQ_HIP(timed(L, GSQ_KERNEL_BACKWARD, stream, [&] { return gsq::launch_backward(L, a, p->lr_scales > 0.f, stream); }));
-  if (loss_out) GSQ_HIP(timed(L, GSQ_KERNEL_REDUCE, stream, [&] { return gsq::launch_reduce_loss(L, loss_out, true, 1.0 / M, stream); }));
+  if (loss_out)
+    GSQ_HIP(timed(L, GSQ_KERNEL_REDUCE, stream, [&] {
+      return gsq::launch_reduce_loss(L, lb.part, lb.stage, lb.tickets, loss_out, true, 1.0 / M, stream);
+    }));
 
   L.last = use;
   L.last_sample = M - 1;
@@ -403,6 +449,63 @@ gsq_status gsq_step(gsq_layer* h, const gsq_step_params* p, float* loss_out, hip
     L.r_valid = false;
   }
   return GSQ_OK;
+}
+
+gsq_status gsq_step(gsq_layer* h, const gsq_step_params* p, float* loss_out, hipStream_t stream) {
+  g_err.clear();
+  if (!h) return fail(GSQ_EINVAL, "handle is NULL");
+  gsq_status st = validate_params(h, p);
+  if (st != GSQ_OK) return st;
+  gsq::Layer& L = *h;
+  if (L.t >= (int64_t)UINT32_MAX) return fail(GSQ_EINVAL, "step counter exhausted");
+  // grow the per-sample buffers before any launch argument captures their addresses
+  const int M = p->samples > 1 ? p->samples : 1;
+  if (M > L.sample_slots) {
+    gsq_status st2 = grow_sample_slots(L, M);
+    if (st2 != GSQ_OK) return st2;
+  }
+  return step_impl(L, p, loss_out, LossBuffers{L.loss_part, L.loss_stage, L.loss_tickets}, stream);
+}
+
+gsq_status gsq_step_static(gsq_layer* h, const gsq_step_params* p, float* loss_out,
+                           hipStream_t stream) {
+  g_err.clear();
+  if (!h) return fail(GSQ_EINVAL, "handle is NULL");
+  gsq_status st = validate_params(h, p);
+  if (st != GSQ_OK) return st;
+  gsq::Layer& L = *h;
+  if (L.t >= (int64_t)UINT32_MAX) return fail(GSQ_EINVAL, "step counter exhausted");
+  const int M = p->samples > 1 ? p->samples : 1;
+  if (M > L.sample_slots)
+    return fail(GSQ_EINVAL,
+                "gsq_step_static allocates nothing: %d samples need per-sample buffers this handle "
+                "does not have yet (it has %d; a gsq_step with that many samples creates them)",
+                M, L.sample_slots);
+  LossBuffers lb{nullptr, nullptr, nullptr};
+  if (loss_out) {
+    const int64_t np = gsq::loss_row_partials(L), ns = gsq::loss_row_stage(L);
+    if (np > (int64_t)kStaticPartials || ns > (int64_t)kStaticStage || L.B > (int64_t)kStaticTickets)
+      return fail(GSQ_EINVAL,
+                  "gsq_step_static's scratch holds %zu loss partials, %zu chunk sums and %zu layers; "
+                  "this layer needs %lld, %lld and %lld (use gsq_step)",
+                  kStaticPartials, kStaticStage, kStaticTickets, (long long)np, (long long)ns,
+                  (long long)L.B);
+    int dev = -1;
+    GSQ_HIP(hipGetDevice(&dev));
+    if (dev != L.device)
+      return fail(GSQ_EINVAL, "the handle was created on device %d, device %d is current", L.device, dev);
+    void* base = nullptr;
+    {
+      std::lock_guard<std::mutex> lock(g_scratch_mu);
+      base = dev >= 0 && dev < kMaxDevices ? g_scratch_ptr[dev] : nullptr;
+    }
+    if (!base) return fail(GSQ_EHIP, "the static scratch of device %d could not be set up", dev);
+    unsigned char* b8 = static_cast<unsigned char*>(base);
+    lb.part = reinterpret_cast<double*>(b8);
+    lb.stage = reinterpret_cast<double*>(b8 + kStaticPartials * 8);
+    lb.tickets = reinterpret_cast<unsigned*>(b8 + (kStaticPartials + kStaticStage) * 8);
+  }
+  return step_impl(L, p, loss_out, lb, stream);
 }
 
 gsq_status gsq_harden(gsq_layer* h, uint8_t* codes, float* scales, float* hard_loss_out,

@@ -481,13 +481,24 @@ int64_t loss_stage_size(const Layer& L) {
   return L.B * ((most + kChunk - 1) / kChunk);
 }
 
+int64_t loss_row_partials(const Layer& L) { return L.B * L.O * L.loss_cols; }
+
+int64_t loss_row_stage(const Layer& L) {
+  return L.B * ((L.O * L.loss_cols + kChunk - 1) / kChunk);
+}
+
 hipError_t launch_reduce_loss(const Layer& L, float* loss_out, bool from_rows, double scale,
                               hipStream_t s) {
-  const double* part = from_rows ? L.loss_part : L.partials;
+  return launch_reduce_loss(L, from_rows ? L.loss_part : L.partials, L.loss_stage, L.loss_tickets,
+                            loss_out, from_rows, scale, s);
+}
+
+hipError_t launch_reduce_loss(const Layer& L, const double* part, double* stage, unsigned* tickets,
+                              float* loss_out, bool from_rows, double scale, hipStream_t s) {
   const int64_t per_batch = from_rows ? L.O * L.loss_cols : contract_tiles_per_batch(L);
   const int nchunks = (int)((per_batch + kChunk - 1) / kChunk);
   hipLaunchKernelGGL(k_reduce_loss, dim3((unsigned)nchunks, (unsigned)L.B), dim3(256), 0, s, part,
-                     per_batch, nchunks, L.loss_stage, L.loss_tickets, scale, loss_out, L.flag);
+                     per_batch, nchunks, stage, tickets, scale, loss_out, L.flag);
   return hipGetLastError();
 }
 

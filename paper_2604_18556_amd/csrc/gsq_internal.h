@@ -87,6 +87,7 @@ struct Layer {
   uint8_t* codes = nullptr;
   uint8_t* J0 = nullptr;       // local shift: initial grid indices
   int64_t t = 0;
+  int device = 0;         // HIP device the handle was created on
   int cur = 0;            // R buffer holding a prepared sample (when r_valid)
   bool r_valid = false;
   int64_t r_t = -1;
@@ -133,5 +134,11 @@ hipError_t launch_contract(const Layer& L, const void* R, bool want_loss, int sl
 // backward's row partials, times `scale`.
 hipError_t launch_reduce_loss(const Layer& L, float* loss_out, bool from_rows, double scale,
                               hipStream_t s);
+// The same with caller-chosen buffers: partials, chunk sums (>= the stage size of the reduction)
+// and one ticket per layer (zero on entry, left at zero).
+hipError_t launch_reduce_loss(const Layer& L, const double* part, double* stage, unsigned* tickets,
+                              float* loss_out, bool from_rows, double scale, hipStream_t s);
+int64_t loss_row_partials(const Layer& L);   // doubles written by the backward's loss terms
+int64_t loss_row_stage(const Layer& L);      // chunk sums of their reduction
 
 }  // namespace gsq

@@ -1,0 +1,88 @@
+"""gsq_step_static, the step that allocates nothing (its loss-reduction scratch is a static device
+array of the library), against gsq_step on twin handles: two layers in a row, the second smaller,
+so the shared scratch is reused with a smaller footprint.  The two entry points run the same
+kernels with the same fixed-order loss reduction, so losses, updated state and intermediates must
+agree bit for bit; a request that would need an allocation is refused before anything runs."""
+import numpy as np
+import pytest
+
+from oracle import gsq as ref
+from paper_2604_18556_amd import binding as B
+from paper_2604_18556_amd import inputs
+
+from gpu_common import Pair, layer_inputs
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+# precision, batch, O, I, levels, gs: the first has 3 x 2000 row partials per layer (several
+# chunks of the reduction), the second is smaller
+CASES = [("bf16", 2, 3000, 512, inputs.L4, 128), ("fp32", 1, 70, 384, inputs.L3, 64)]
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.load()
+    return torch.device("cuda:0")
+
+
+def _same_state(a, b, label):
+    sa, sb = a.get(), b.get()
+    for k in ("logits", "m", "v", "scales", "m_s", "v_s"):
+        np.testing.assert_array_equal(getattr(sa, k), getattr(sb, k), err_msg=f"{label} {k}")
+    assert sa.t == sb.t
+    Ra, Ga = a.intermediates()
+    Rb, Gb = b.intermediates()
+    np.testing.assert_array_equal(Ra, Rb, err_msg=f"{label} R")
+    np.testing.assert_array_equal(Ga, Gb, err_msg=f"{label} G")
+
+
+def test_static_step_equals_gsq_step_on_two_layers_in_a_row(dev):
+    for prec, batch, O, I, levels, gs in CASES:
+        label = f"{prec} {batch}x{O}x{I}"
+        print(f"no-alloc step: {label}", flush=True)
+        W, H = layer_inputs(O, I, batch=batch, bf16=prec == "bf16", seed=O)
+        rcfg = ref.Config(O, I, levels, gs, batch=batch, precision=prec, seed=3)
+        a, b = Pair(rcfg, W, H, dev), Pair(rcfg, W, H, dev)
+        taus = [0.8, 0.5, 0.3]
+        for t in range(3):
+            # fused next sample on the first two steps, the loss on all but the second
+            prm = B.StepParams(tau=taus[t], tau_next=taus[t + 1] if t + 1 < 3 else 0.0)
+            want = t != 1
+            la = torch.full((batch,), -1.0, device=dev) if want else None
+            lb = torch.full((batch,), -2.0, device=dev) if want else None
+            a.layer.step(prm, loss_out=la)
+            b.layer.step_static(prm, loss_out=lb)
+            torch.cuda.synchronize()
+            if want:
+                np.testing.assert_array_equal(la.cpu().numpy(), lb.cpu().numpy(), err_msg=label)
+                assert np.all(np.isfinite(lb.cpu().numpy())) and np.all(lb.cpu().numpy() > 0)
+        _same_state(a, b, label)
+        a.layer.check()
+        b.layer.check()
+        a.layer.destroy()
+        b.layer.destroy()
+
+
+def test_static_step_refuses_what_would_allocate(dev):
+    W, H = layer_inputs(40, 256, seed=9)
+    rcfg = ref.Config(40, 256, inputs.L4, 128, precision="bf16", seed=1)
+    a, b = Pair(rcfg, W, H, dev), Pair(rcfg, W, H, dev)
+    # a new handle has one sample slot: two samples would need new gradient buffers
+    with pytest.raises(B.GsqError) as e:
+        b.layer.step_static(B.StepParams(tau=0.5, samples=2))
+    assert e.value.status == B.GSQ_EINVAL
+    assert "allocates nothing" in str(e.value)
+    # after gsq_step has created them, the static step may use them, with identical results
+    a.layer.step(B.StepParams(tau=0.5, samples=2))
+    b.layer.step(B.StepParams(tau=0.5, samples=2))
+    la, lb = torch.zeros(1, device=dev), torch.zeros(1, device=dev)
+    a.layer.step(B.StepParams(tau=0.4, samples=2), loss_out=la)
+    b.layer.step_static(B.StepParams(tau=0.4, samples=2), loss_out=lb)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(la.cpu().numpy(), lb.cpu().numpy())
+    _same_state(a, b, "two samples")
+    a.layer.destroy()
+    b.layer.destroy()
