@@ -13,9 +13,9 @@ and synthetic and resident in HBM before timing starts.
 
 Prints one JSON line: steps/s, the roofline of the dominant kernel (its duration measured
 with HIP events on the library's stream during the timed steps), the CPU oracle timed on a
-bounded sample of the same workload, and (key "target_layer") the kernel rooflines of a
-short run on the 4096 x 14336 MLP down projection, whose contraction is the matrix-core
-target.
+bounded sample of the same workload, (key "target_layer") the kernel rooflines of a short
+run on the 4096 x 14336 MLP down projection, whose contraction is the matrix-core target, and
+(key "local_shift_variant") a short run of the same experts under the local-shift relaxation.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
     python bench.py --copy-calibration   # plain device copy of known size, for PMC scaling
@@ -36,6 +36,7 @@ PEAK_BF16_TFLOPS = 2500.0      # dense bf16 MFMA
 PEAK_FP64_TFLOPS = 78.6        # fp64 vector (the FP32 precision accumulates in fp64)
 DEFAULT_WORKLOAD = "moe-64x2048x7168-superblock"
 TARGET_LAYER = "mlp-down-4096x14336-k8"   # the layer the matrix-core target names
+VARIANT_OF = {"moe-64x2048x7168-superblock": "moe-64x2048x7168-superblock-shift8"}
 ONCE_REPS = 5                  # timed calls of gsq_harden / gsq_pack
 
 
@@ -261,9 +262,10 @@ def tau_at(t, T):
     return 1.0 + (0.05 - 1.0) * t / (T - 1)
 
 
-def target_layer(name, dev, steps=10, warmup=3):
-    """Kernel rooflines of a short run (``steps`` timed steps after ``warmup``) on the layer the
-    matrix-core target names: each launch between the library's HIP events on its stream."""
+def short_run(name, dev, steps=10, warmup=3):
+    """A short run of another workload (same schedule, fused next sample, loss every step):
+    steps/s over ``steps`` timed steps after ``warmup``, then the kernel rooflines of the next
+    ``steps`` steps, each launch between the library's HIP events on its stream."""
     import torch
     from paper_2604_18556_amd import binding as B
     from paper_2604_18556_amd import inputs
@@ -273,23 +275,32 @@ def target_layer(name, dev, steps=10, warmup=3):
     layer = B.Layer(make_config(B, w), Wd, Hd)
     del W, Wd, Hd
     loss = torch.zeros(w.batch, device=dev)
-    for i in range(warmup + steps):
-        if i == warmup:
-            layer.timing(True)
-            layer.timing_read(reset=True)
-        layer.step(B.StepParams(tau=tau_at(i, w.steps), lr_scales=w.lr_scales,
-                                tau_next=tau_at(i + 1, w.steps)), loss_out=loss)
+
+    def run(t0, n):
+        for t in range(t0, t0 + n):
+            layer.step(B.StepParams(tau=tau_at(t, w.steps), lr_scales=w.lr_scales,
+                                    tau_next=tau_at(t + 1, w.steps)), loss_out=loss)
+    run(0, warmup)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    run(warmup, steps)
+    end.record()
+    torch.cuda.synchronize()
+    ms_step = start.elapsed_time(end) / steps
+    layer.timing(True)
+    layer.timing_read(reset=True)
+    run(warmup + steps, steps)
     kern = layer.timing_read(reset=True)
     layer.check()
     layer.destroy()
     per_kernel = kernel_table(kern, algorithmic_work(w, True, True, w.lr_scales), w, steps)
-    out = {"workload": name, "steps": steps, "warmup": warmup}
+    out = {"workload": name, "value": 1e3 / ms_step, "unit": "steps/s", "ms_per_step": ms_step,
+           "steps": steps, "warmup": warmup}
     for k in ("contract", "backward"):
         e = per_kernel[k]
         out[k] = {key: e[key] for key in ("avg_ms", "bound", "achieved", "peak", "unit", "frac")}
         out[k]["traffic"] = measured_traffic(k, name)
-    out["note"] = ("the contraction's matrix-core fraction (bf16 peak 2.5 PFLOP/s) and the "
-                   "backward's HBM fraction on this layer; steps of the same schedule")
     return out
 
 
@@ -313,6 +324,9 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--target-layer", default=TARGET_LAYER,
                     help="workload of the short extra run reported under target_layer ('' skips it)")
+    ap.add_argument("--variant", default=None,
+                    help="workload of a second short run reported under local_shift_variant "
+                         "(default: the local-shift form of the default MoE workload; '' skips it)")
     ap.add_argument("--optimizer", choices=("adam", "lion"), default="adam",
                     help="adam (default) or lion (the paper's optimiser; lr 1e-4, weight decay 1.0)")
     ap.add_argument("--samples", type=int, default=1,
@@ -336,6 +350,8 @@ def main():
         return
 
     w = inputs.WORKLOADS[args.workload]
+    if args.variant is None:
+        args.variant = VARIANT_OF.get(w.name, "")
     W, Hd = inputs.make_layer(w, device=dev)
     Wd = torch.from_numpy(W).to(dev)
     if w.precision == "bf16":
@@ -424,9 +440,17 @@ def main():
             lib_gemm = {"error": str(ex)[:200]}
 
     layer.destroy()
-    target = None
+    del Wd
+    target = variant = None
     if args.target_layer and args.target_layer != w.name:
-        target = target_layer(args.target_layer, dev)
+        target = short_run(args.target_layer, dev)
+        target["note"] = ("the layer the matrix-core target names: its contraction's fraction of "
+                          "the bf16 peak (2.5 PFLOP/s) and the backward's of the HBM peak")
+    if args.variant and args.variant != w.name:
+        variant = short_run(args.variant, dev)
+        variant["note"] = ("the same experts with the local-shift relaxation (5 logits over "
+                           "shifts of the round-to-nearest index), App. E's procedure for "
+                           "K-quant sets of more than four values")
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -474,6 +498,7 @@ def main():
                                    "first re-derives the codes (pack_harden_ms)"},
         "library_gemm": lib_gemm,
         "target_layer": target,
+        "local_shift_variant": variant,
         "gpu_vs_cpu": None if cpu is None else (1e3 / ms_step) / cpu["value"],
     }
     print(json.dumps(out), flush=True)
