@@ -45,10 +45,19 @@ def short(name):
     return name[:70]
 
 
-def per_kernel_counters(path):
+def per_kernel_counters(path, steps_only=False):
+    """{(kernel, counter): (mean per dispatch, dispatches)}.  With steps_only, only the dispatches
+    before the first harden kernel count: the optimisation steps, not gsq_harden's hard-loss
+    contractions."""
+    rows = list(csv.DictReader(open(path)))
+    cut = float("inf")
+    if steps_only:
+        cut = min((int(r["Dispatch_Id"]) for r in rows if short(r["Kernel_Name"]) == "harden"),
+                  default=float("inf"))
     agg = collections.defaultdict(list)
-    for r in csv.DictReader(open(path)):
-        agg[(short(r["Kernel_Name"]), r["Counter_Name"])].append(float(r["Counter_Value"]))
+    for r in rows:
+        if int(r["Dispatch_Id"]) < cut:
+            agg[(short(r["Kernel_Name"]), r["Counter_Name"])].append(float(r["Counter_Value"]))
     return {k: (sum(v) / len(v), len(v)) for k, v in agg.items()}
 
 
@@ -124,8 +133,8 @@ def cmd_mfma(a):
 
 
 def cmd_traffic(a):
-    f = per_kernel_counters(a.fetch)
-    w = per_kernel_counters(a.write)
+    f = per_kernel_counters(a.fetch, steps_only=True)
+    w = per_kernel_counters(a.write, steps_only=True)
     cf = per_kernel_counters(a.copy_fetch)
     cw = per_kernel_counters(a.copy_write)
     copy_kib = a.copy_bytes / 1024.0
@@ -137,7 +146,8 @@ def cmd_traffic(a):
     wk = w[(a.kernel, "WRITE_SIZE")][0] * sw * 1024
     src = KERNEL_MATCH[a.kernel][1]
     sha = hashlib.sha256(open(os.path.join(PKG, "csrc", src), "rb").read()).hexdigest()
-    print(f"# HBM traffic of one {a.kernel} launch, workload {a.workload}\n# command: {a.cmd}\n")
+    print(f"# HBM traffic of one {a.kernel} launch of the optimisation steps, workload {a.workload}"
+          f"\n# command: {a.cmd}\n")
     print(f"copy calibration: {a.copy_bytes} bytes read and written; FETCH_SIZE scale {sf:.4f}, "
           f"WRITE_SIZE scale {sw:.4f}")
     print(f"{a.kernel}: FETCH_SIZE {f[(a.kernel, 'FETCH_SIZE')][0]:.1f} KiB/dispatch -> {fk / 1e6:.2f} MB")
