@@ -68,6 +68,18 @@ struct Split {
   float* ws;    // (tiles - full) x split x 256 x 256 fp32
 };
 
+// Batches of layers (MoE experts): the tiles of each layer are grouped into blocks of bm x bn
+// tiles (bm tile rows, bn tile columns, bm bn <= 32), one block per XCD at a time, so that the
+// 32 CUs of an XCD work on one layer's 32 tiles together and its L2 holds bm R panels and bn H
+// panels for them.  Block q goes to XCD q mod 8 (workgroup w runs on XCD w mod 8); the XCD's
+// workgroups take its blocks in turn, 32 per block.
+struct XcdBlocks {
+  int on;
+  int bm, bn;       // block shape in tiles
+  int nbr, nbc;     // blocks per layer: rows, columns
+  int nblocks;      // over all layers
+};
+
 // One 256 x 256 tile of G per workgroup; four wavefronts each own 128 x 128 as 4 x 4 MFMA
 // 32x32x16 tiles.  K slabs 64 wide (whole 128-byte lines of R and H) move by direct global->LDS
 // loads (16 bytes per lane, no staging registers) into a ring of three buffers for R and two for
@@ -123,23 +135,36 @@ __global__ __launch_bounds__(256, 1) void k_contract_bf16(const uint16_t* __rest
                                                           float* __restrict__ G,
                                                           double* __restrict__ partials,
                                                           int64_t Opad, int64_t Ipad, int tiles_m,
-                                                          int tiles_n, int want_loss, Split sp) {
+                                                          int tiles_n, int want_loss, Split sp,
+                                                          XcdBlocks xb) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-  const int64_t b = blockIdx.z;
+  int64_t b = blockIdx.z;
   int nk = (int)(Ipad / BK);   // a multiple of 4 (Ipad is a multiple of 256)
-  int lin, part = -1, kb = 0;
-  if ((int)blockIdx.x < sp.full) {
-    lin = lin_of(blockIdx.x, sp.full);
-  } else {   // a K part of a tile of the last round (XCD-contiguous numbering as well)
-    const int nq = (int)gridDim.x - sp.full;
-    const int q = lin_of(blockIdx.x - sp.full, nq);
-    lin = sp.full + q / sp.split;
-    part = q % sp.split;
-    nk /= sp.split;
-    kb = part * nk;
-  }
+  int lin = 0, part = -1, kb = 0;
   int tm, tn;
-  tile_at(lin, tiles_m, tiles_n, tm, tn);
+  if (xb.on) {
+    const int x = blockIdx.x & 7, k = blockIdx.x >> 3;
+    const int q = (k >> 5) * 8 + x, j = k & 31;
+    if (q >= xb.nblocks || j >= xb.bm * xb.bn) return;   // whole workgroup
+    const int per_layer = xb.nbr * xb.nbc;
+    b = q / per_layer;
+    const int r = q - (int)b * per_layer;
+    tm = (r / xb.nbc) * xb.bm + j % xb.bm;
+    tn = (r % xb.nbc) * xb.bn + j / xb.bm;
+    if (tm >= tiles_m || tn >= tiles_n) return;
+  } else {
+    if ((int)blockIdx.x < sp.full) {
+      lin = lin_of(blockIdx.x, sp.full);
+    } else {   // a K part of a tile of the last round (XCD-contiguous numbering as well)
+      const int nq = (int)gridDim.x - sp.full;
+      const int q = lin_of(blockIdx.x - sp.full, nq);
+      lin = sp.full + q / sp.split;
+      part = q % sp.split;
+      nk /= sp.split;
+      kb = part * nk;
+    }
+    tile_at(lin, tiles_m, tiles_n, tm, tn);
+  }
   const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
   const uint16_t* A = R + b * Opad * Ipad + m0 * Ipad + (int64_t)kb * BK;
   const uint16_t* Bt = H + b * Ipad * Ipad + n0 * Ipad + (int64_t)kb * BK;
@@ -435,9 +460,19 @@ hipError_t launch_contract(const Layer& L, const void* R, bool want_loss, int sl
     Split sp{tiles, 1, nullptr};
     if (L.split_parts > 1 && !want_loss) sp = Split{L.split_full, L.split_parts, L.split_ws};
     dim3 grid((unsigned)(sp.full + (tiles - sp.full) * sp.split), 1, (unsigned)L.B);
+    XcdBlocks xb{0, 0, 0, 0, 0, 0};
+    if (L.B > 1) {   // one layer's block of tiles per XCD at a time
+      xb.on = 1;
+      xb.bm = std::min(tiles_m, 8);
+      xb.bn = std::min(tiles_n, 32 / xb.bm);
+      xb.nbr = (tiles_m + xb.bm - 1) / xb.bm;
+      xb.nbc = (tiles_n + xb.bn - 1) / xb.bn;
+      xb.nblocks = (int)L.B * xb.nbr * xb.nbc;
+      grid = dim3((unsigned)(8 * 32 * ((xb.nblocks + 7) / 8)), 1, 1);
+    }
     hipLaunchKernelGGL(k_contract_bf16, grid, dim3(256), LDS_BYTES, s,
                        static_cast<const uint16_t*>(R), static_cast<const uint16_t*>(L.H), G,
-                       partials, L.Opad, L.Ipad, tiles_m, tiles_n, want_loss ? 1 : 0, sp);
+                       partials, L.Opad, L.Ipad, tiles_m, tiles_n, want_loss ? 1 : 0, sp, xb);
     if (sp.split > 1) {
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
