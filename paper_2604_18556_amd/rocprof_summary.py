@@ -161,6 +161,22 @@ def cmd_traffic(a):
         json.dump(data, open(a.json, "w"), indent=1, sort_keys=True)
 
 
+def cmd_l2(a):
+    """L2 (TCC) hit rate and the bytes read past the L2 (TCC_EA0_RDREQ_DRAM_32B x 32) per step
+    dispatch of the step kernels, beside the algorithmic R + H bytes of the contraction."""
+    c = per_kernel_counters(a.csv, steps_only=True)
+    print(f"# L2 counters per step dispatch\n# command: {a.cmd}\n")
+    print(f"{'kernel':<10} {'L2 hit':>7} {'requests':>12} {'read past L2 MB':>16}")
+    for k in ("contract", "backward"):
+        if (k, "TCC_HIT_sum") not in c:
+            continue
+        hit, miss = c[(k, "TCC_HIT_sum")][0], c[(k, "TCC_MISS_sum")][0]
+        rd = c[(k, "TCC_EA0_RDREQ_DRAM_32B_sum")][0] * 32
+        print(f"{k:<10} {hit / (hit + miss):>7.3f} {hit + miss:>12.4g} {rd / 1e6:>16.1f}")
+    if a.rh_bytes:
+        print(f"\ncontraction operands R + H: {a.rh_bytes / 1e6:.1f} MB per step")
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="what", required=True)
@@ -174,6 +190,10 @@ def main(argv=None):
     m.add_argument("csv")
     m.add_argument("--agent", required=True)
     m.add_argument("--cmd", default="")
+    l2 = sub.add_parser("l2")
+    l2.add_argument("csv")
+    l2.add_argument("--rh-bytes", type=float, default=0.0)
+    l2.add_argument("--cmd", default="")
     t = sub.add_parser("traffic")
     for k in ("fetch", "write", "copy_fetch", "copy_write", "kernel", "workload"):
         t.add_argument("--" + k.replace("_", "-"), dest=k, required=True)
@@ -181,7 +201,8 @@ def main(argv=None):
     t.add_argument("--json")
     t.add_argument("--cmd", default="")
     a = ap.parse_args(argv)
-    {"stats": cmd_stats, "pmc": cmd_pmc, "mfma": cmd_mfma, "traffic": cmd_traffic}[a.what](a)
+    {"stats": cmd_stats, "pmc": cmd_pmc, "mfma": cmd_mfma, "traffic": cmd_traffic,
+     "l2": cmd_l2}[a.what](a)
 
 
 if __name__ == "__main__":
