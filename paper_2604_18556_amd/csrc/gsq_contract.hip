@@ -130,6 +130,82 @@ __device__ __forceinline__ void slab_barrier() {
 // scheduling-group masks
 constexpr int SG_MFMA = 0x008, SG_VMEM = 0x020, SG_DSR = 0x100;
 
+// Epilogue of a tile: the raw P of a split tile's K part into the workspace, else G = -2 P and,
+// on request, the tile's loss partial sum(R P).
+// 32 x 32 accumulator layout: lane l, register r -> row 8*(r/4) + 4*(l/32) + r%4, column l%32.
+__device__ __forceinline__ void finish_tile(f32x16 (&acc)[4][4], const uint16_t* R, float* G,
+                                            double* partials, int64_t Opad, int64_t Ipad,
+                                            int tiles_m, int tiles_n, int want_loss,
+                                            const Split& sp, int64_t b, int tm, int tn, int part,
+                                            int lin, int wm, int wn, int lane, uint8_t* smem) {
+  const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
+  if (part >= 0) {   // raw P of this K part, tile-local row-major
+    float* W_ = sp.ws + ((int64_t)(lin - sp.full) * sp.split + part) * (BM * BN);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          W_[(wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * BN + wn * 128 + j * 32 +
+             (lane & 31)] = acc[i][j][r];
+    return;
+  }
+  float* Gb = G + b * Opad * Ipad;
+  const uint16_t* Rb = R + b * Opad * Ipad;
+  double lsum = 0.0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t row = m0 + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        const int64_t col = n0 + wn * 128 + j * 32 + (lane & 31);
+        const float p = acc[i][j][r];
+        Gb[row * Ipad + col] = -2.f * p;
+        if (want_loss) lsum += (double)bf16_to_f32(Rb[row * Ipad + col]) * (double)p;
+      }
+  if (want_loss)
+    block_sum_to(lsum, partials + b * (int64_t)tiles_m * tiles_n + tm * tiles_n + tn,
+                 reinterpret_cast<double*>(smem));
+}
+
+// The tile of this workgroup: layer b, tile row tm, tile column tn, and for a split tile of the
+// last round its K part (part >= 0) as slabs kb .. kb + nk - 1.  False: no tile (whole group).
+__device__ __forceinline__ bool pick_tile(int tiles_m, int tiles_n, int64_t Ipad, const Split& sp,
+                                          const XcdBlocks& xb, int64_t& b, int& tm, int& tn,
+                                          int& part, int& kb, int& nk, int& lin) {
+  b = blockIdx.z;
+  nk = (int)(Ipad / BK);   // a multiple of 4 (Ipad is a multiple of 256)
+  lin = 0;
+  part = -1;
+  kb = 0;
+  if (xb.on) {
+    const int x = blockIdx.x & 7, k = blockIdx.x >> 3;
+    const int q = (k >> 5) * 8 + x, j = k & 31;
+    if (q >= xb.nblocks || j >= xb.bm * xb.bn) return false;
+    const int per_layer = xb.nbr * xb.nbc;
+    b = q / per_layer;
+    const int r = q - (int)b * per_layer;
+    tm = (r / xb.nbc) * xb.bm + j % xb.bm;
+    tn = (r % xb.nbc) * xb.bn + j / xb.bm;
+    return tm < tiles_m && tn < tiles_n;
+  }
+  if ((int)blockIdx.x < sp.full) {
+    lin = lin_of(blockIdx.x, sp.full);
+  } else {   // a K part of a tile of the last round (XCD-contiguous numbering as well)
+    const int nq = (int)gridDim.x - sp.full;
+    const int q = lin_of(blockIdx.x - sp.full, nq);
+    lin = sp.full + q / sp.split;
+    part = q % sp.split;
+    nk /= sp.split;
+    kb = part * nk;
+  }
+  tile_at(lin, tiles_m, tiles_n, tm, tn);
+  return true;
+}
+
 __global__ __launch_bounds__(256, 1) void k_contract_bf16(const uint16_t* __restrict__ R,
                                                           const uint16_t* __restrict__ H,
                                                           float* __restrict__ G,
@@ -138,33 +214,9 @@ __global__ __launch_bounds__(256, 1) void k_contract_bf16(const uint16_t* __rest
                                                           int tiles_n, int want_loss, Split sp,
                                                           XcdBlocks xb) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-  int64_t b = blockIdx.z;
-  int nk = (int)(Ipad / BK);   // a multiple of 4 (Ipad is a multiple of 256)
-  int lin = 0, part = -1, kb = 0;
-  int tm, tn;
-  if (xb.on) {
-    const int x = blockIdx.x & 7, k = blockIdx.x >> 3;
-    const int q = (k >> 5) * 8 + x, j = k & 31;
-    if (q >= xb.nblocks || j >= xb.bm * xb.bn) return;   // whole workgroup
-    const int per_layer = xb.nbr * xb.nbc;
-    b = q / per_layer;
-    const int r = q - (int)b * per_layer;
-    tm = (r / xb.nbc) * xb.bm + j % xb.bm;
-    tn = (r % xb.nbc) * xb.bn + j / xb.bm;
-    if (tm >= tiles_m || tn >= tiles_n) return;
-  } else {
-    if ((int)blockIdx.x < sp.full) {
-      lin = lin_of(blockIdx.x, sp.full);
-    } else {   // a K part of a tile of the last round (XCD-contiguous numbering as well)
-      const int nq = (int)gridDim.x - sp.full;
-      const int q = lin_of(blockIdx.x - sp.full, nq);
-      lin = sp.full + q / sp.split;
-      part = q % sp.split;
-      nk /= sp.split;
-      kb = part * nk;
-    }
-    tile_at(lin, tiles_m, tiles_n, tm, tn);
-  }
+  int64_t b;
+  int tm, tn, part, kb, nk, lin;
+  if (!pick_tile(tiles_m, tiles_n, Ipad, sp, xb, b, tm, tn, part, kb, nk, lin)) return;
   const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
   const uint16_t* A = R + b * Opad * Ipad + m0 * Ipad + (int64_t)kb * BK;
   const uint16_t* Bt = H + b * Ipad * Ipad + n0 * Ipad + (int64_t)kb * BK;
@@ -269,37 +321,8 @@ __global__ __launch_bounds__(256, 1) void k_contract_bf16(const uint16_t* __rest
 #undef GSQ_ISSUE_A
 #undef GSQ_ISSUE_B
 
-  // 32 x 32 accumulator layout: lane l, register r -> row 8*(r/4) + 4*(l/32) + r%4, column l%32
-  if (part >= 0) {   // raw P of this K part, tile-local row-major
-    float* W_ = sp.ws + ((int64_t)(lin - sp.full) * sp.split + part) * (BM * BN);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          W_[(wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * BN + wn * 128 + j * 32 +
-             (lane & 31)] = acc[i][j][r];
-    return;
-  }
-  float* Gb = G + b * Opad * Ipad;
-  const uint16_t* Rb = R + b * Opad * Ipad;
-  double lsum = 0.0;
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t row = m0 + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        const int64_t col = n0 + wn * 128 + j * 32 + (lane & 31);
-        const float p = acc[i][j][r];
-        Gb[row * Ipad + col] = -2.f * p;
-        if (want_loss) lsum += (double)bf16_to_f32(Rb[row * Ipad + col]) * (double)p;
-      }
-  if (want_loss)
-    block_sum_to(lsum, partials + b * (int64_t)tiles_m * tiles_n + tm * tiles_n + tn,
-                 reinterpret_cast<double*>(smem));
+  finish_tile(acc, R, G, partials, Opad, Ipad, tiles_m, tiles_n, want_loss, sp, b, tm, tn, part, lin,
+              wm, wn, lane, smem);
 }
 
 // G = -2 (P_0 + ... + P_{split-1}) for the split tiles of the last round, parts added in order.
