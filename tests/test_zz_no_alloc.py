@@ -86,3 +86,23 @@ def test_static_step_refuses_what_would_allocate(dev):
     _same_state(a, b, "two samples")
     a.layer.destroy()
     b.layer.destroy()
+
+
+def test_static_step_refuses_a_layer_beyond_its_scratch(dev):
+    """A layer with more loss partials than the static scratch holds (4194304: one per row and
+    256 columns) is refused with GSQ_EINVAL before anything runs; without a loss the same layer
+    needs no scratch and steps."""
+    O, I = 4_194_305, 16
+    cfg = B.LayerConfig(O, I, inputs.L4, 16, precision=B.PREC_BF16, seed=2, init_noise=False)
+    W = torch.full((1, O, I), 0.01, dtype=torch.bfloat16, device=dev)
+    H = torch.eye(I, device=dev).unsqueeze(0)
+    layer = B.Layer(cfg, W, H)
+    del W
+    loss = torch.zeros(1, device=dev)
+    with pytest.raises(B.GsqError) as e:
+        layer.step_static(B.StepParams(tau=0.5), loss_out=loss)
+    assert e.value.status == B.GSQ_EINVAL
+    assert "4194304" in str(e.value)
+    layer.step_static(B.StepParams(tau=0.5))
+    layer.check()
+    layer.destroy()
