@@ -353,7 +353,7 @@ def test_superblock_rejects_scale_training(dev):
 # ------------------------------------------------------------------ full size, sampled rows
 FULL_SIZE = ["attn-4096x4096-k3", "attn-4096x4096-ternary", "mlp-up-14336x4096-k8",
              "mlp-down-4096x14336-k8", "mlp-down-4096x14336-shift8", "down-8192x28672-k4",
-             "moe-64x2048x7168-superblock"]
+             "moe-64x2048x7168-superblock", "moe-64x2048x7168-superblock-shift8"]
 
 
 @pytest.mark.parametrize("name", FULL_SIZE)

@@ -136,6 +136,36 @@ def test_single_step_matches_oracle(dev, relax, prec, O, I, levels, gs, tau, kap
         np.testing.assert_array_equal(got.base, st.base)   # the base never moves
 
 
+@pytest.mark.parametrize("prec,batch,O,I,gs,layout", [("bf16", 2, 48, 512, 16, "superblock"),
+                                                       ("fp32", 1, 70, 384, 64, "group"),
+                                                       ("bf16", 1, 130, 272, 16, "group")])
+@pytest.mark.parametrize("opt", ["adam", "lion"])
+def test_shift_step_with_frozen_scales(dev, prec, batch, O, I, gs, layout, opt):
+    """The local shift with frozen scales (lr_scales = 0, as for the super-block experts), whose
+    backward keeps every moment in flight (a code path of its own), from warm moments and any
+    base indices, under Adam and Lion."""
+    W, H = layer_inputs(O, I, batch=batch, bf16=prec == "bf16", seed=O + I)
+    rcfg = ref.Config(O, I, L8, gs, batch=batch, layout=layout, precision=prec, seed=8,
+                      relaxation="shift")
+    pair = Pair(rcfg, W, H, dev)
+    rng = np.random.default_rng(I)
+    st = warm_state(ref.init_layer(rcfg, W), rng)
+    st.base = rng.integers(0, 8, st.base.shape).astype(np.uint8)
+    pair.put(st)
+    kw = dict(optimizer=B.OPT_LION, lr_logits=1e-3, weight_decay=1.0) if opt == "lion" else {}
+    prm = B.StepParams(tau=0.3, lr_scales=0.0, **kw)
+    loss = pair.step(prm)
+    R, G = pair.intermediates()
+    new, L, inter = ref.step(rcfg, W, pair.Hs, st, oracle_params(prm), want=True)
+    tol = TOL[prec]
+    assert np.all(np.abs(loss - L) <= tol * np.abs(L)), (loss, L)
+    assert rel_err(G, inter["G"]) <= tol
+    got = pair.get()
+    assert_state_close(got, new, inter["G"], tol, st.t + 1, label=f"frozen shift {prec} {O}x{I}",
+                       dlogits=inter["dlogits"])
+    np.testing.assert_array_equal(got.scales, st.scales)
+
+
 @pytest.mark.parametrize("relax,prec", [("shift", "fp32"), ("ternary", "bf16")])
 def test_lion_and_samples_step(dev, relax, prec):
     """The paper's optimiser (Lion, weight decay) and three averaged draws on the relaxations."""
