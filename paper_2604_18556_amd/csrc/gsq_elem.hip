@@ -363,17 +363,17 @@ __device__ __forceinline__ double wave_sum_to_lane63(double x) {
 // block (R rebuilt exactly as the contraction saw it) into a.loss_part.
 // Register budget of the backward.  Updating the moments one logit plane at a time (each
 // plane's m and v loaded just before its update) keeps 8K fewer registers live than loading
-// them all first, at the price of less memory parallelism within a wavefront.  It pays where
-// it buys another wavefront per SIMD: the shift relaxation with trained scales (2 -> 3
-// wavefronts, 5 % faster at 4096 x 14336) and grids of 5 to 7 levels (2 -> 3).  With frozen
-// scales (the super-block MoE) the shift keeps every moment in flight instead: 21.3 -> 19.7 ms
-// on the 64 experts.  The 8-level grids keep every moment in flight at two wavefronts: with the
-// non-temporal state accesses this is 1 % faster on the super-block MoE than the plane-by-plane
-// update under a bound of three wavefronts, and with trained scales that bound spills.  The
-// smaller grids keep all moments in flight as well.
-template <int K, int kMode, bool kScales>
+// them all first, at the price of less memory parallelism within a wavefront.  It buys another
+// wavefront per SIMD (2 -> 3) for grids of 5 to 7 levels, which keep it.  The local shift keeps
+// every moment in flight: with the non-temporal state accesses that is 7-8 % faster than the
+// plane-by-plane update at three wavefronts (4096 x 14336: 1.33 -> 1.23 ms; the MoE experts with
+// frozen scales: 21.3 -> 19.7 ms).  The 8-level grids keep every moment in flight at two
+// wavefronts: 1 % faster on the super-block MoE than the plane-by-plane update under a bound of
+// three wavefronts, and with trained scales that bound spills.  The smaller grids keep all
+// moments in flight as well.
+template <int K, int kMode>
 constexpr bool backward_plane_update() {
-  return (kMode == GSQ_RELAX_SHIFT && kScales) || (kMode == GSQ_RELAX_GRID && K >= 5 && K <= 7);
+  return kMode == GSQ_RELAX_GRID && K >= 5 && K <= 7;
 }
 
 template <int K, bool kF64, bool kScales, bool kMulti, int kMode, bool kLion>
@@ -461,7 +461,7 @@ __global__ __launch_bounds__(kBlock) void k_backward(
     }
     // the moments are needed only by the update: loading them here keeps them out of the
     // registers of the sample loop
-    if constexpr (backward_plane_update<K, kMode, kScales>()) {
+    if constexpr (backward_plane_update<K, kMode>()) {
 #pragma unroll
       for (int k = 0; k < K; ++k) {
         float4 mk = active ? ld_stream(a.M + state_off(e0, k, K))
