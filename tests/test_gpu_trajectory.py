@@ -34,7 +34,7 @@ pytestmark = pytest.mark.gpu
 
 RUNS = ["attn-4096x4096-k3", "attn-4096x4096-ternary", "mlp-up-14336x4096-k8",
         "mlp-down-4096x14336-k8", "mlp-down-4096x14336-shift8", "down-8192x28672-k4",
-        "moe-64x2048x7168-superblock"]
+        "moe-64x2048x7168-superblock", "moe-64x2048x7168-superblock-shift8"]
 GAP_TOL = 1e-4
 RUN_TOL = 5e-3
 CKPT_TOL_G = {"adam": 5e-3, "lion": 2e-2}
