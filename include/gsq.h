@@ -105,7 +105,9 @@ typedef struct {
                               SUPERBLOCK, whose scales stay in their 6-bit grid)            */
   float   beta1, beta2;    /* Adam moment decays, in [0, 1)                                 */
   float   eps;             /* Adam denominator constant (> 0)                               */
-  int32_t gumbel_noise;    /* 1: sample g ~ Gumbel(0,1) (Alg. 1); 0: g = 0                  */
+  int32_t gumbel_noise;    /* 1: sample the noise of Alg. 1 (GRID, SHIFT: g ~ Gumbel(0,1)
+                              per logit; TERNARY: one Logistic(0,1) value per binary pair,
+                              as gsq_gumbel describes); 0: no noise                         */
   float   tau_next;        /* temperature of the NEXT call's step, or 0 if unknown.  When
                               the next call passes exactly (tau_next, kappa_next) the sample
                               of that step has already been drawn by this one, saving one
@@ -117,7 +119,7 @@ typedef struct {
                               + weight_decay theta), then m = beta2 m + (1-beta2) g; eps and
                               the second moment are unused                                   */
   float   weight_decay;    /* decoupled weight decay on logits and scales (>= 0)            */
-  int32_t samples;         /* M independent Gumbel draws this step, 0 or 1 = one draw, at most
+  int32_t samples;         /* M independent noise draws this step, 0 or 1 = one draw, at most
                               GSQ_MAX_SAMPLES: gradients and the reported loss are averaged
                               over the M samples (§3.3, gradient accumulation with resampled
                               noise).  Each extra sample costs one more forward pass and one
