@@ -14,8 +14,10 @@ and synthetic and resident in HBM before timing starts.
 Prints one JSON line: steps/s, the roofline of the dominant kernel (its duration measured
 with HIP events on the library's stream during the timed steps), the CPU oracle timed on a
 bounded sample of the same workload, (key "target_layer") the kernel rooflines of a short
-run on the 4096 x 14336 MLP down projection, whose contraction is the matrix-core target, and
-(key "local_shift_variant") a short run of the same experts under the local-shift relaxation.
+run on the 4096 x 14336 MLP down projection, whose contraction is the matrix-core target,
+(key "local_shift_variant") a short run of the same experts under the local-shift relaxation,
+and (keys "lion_variant", "multi_sample_variant") short runs of the default workload under Lion
+and with two noise draws per step.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
     python bench.py --copy-calibration   # plain device copy of known size, for PMC scaling
@@ -237,13 +239,16 @@ def kernel_table(kern, work, w, steps):
 KERNEL_SOURCE = {"forward": "gsq_elem.hip", "backward": "gsq_elem.hip", "contract": "gsq_contract.hip"}
 
 
-def dominant_roofline(per_kernel, w):
-    """The roofline object of the kernel with the largest time per step."""
+def dominant_roofline(per_kernel, w, profiled=True):
+    """The roofline object of the kernel with the largest time per step.  ``profiled``: the run
+    has the launch configuration of the committed PMC passes (Adam, one sample, the loss every
+    step, the next sample fused), so their measured traffic applies; otherwise it is null."""
     dom = max((k for k in per_kernel if "bound" in per_kernel[k]),
               key=lambda k: per_kernel[k]["ms_per_step"])
     d = per_kernel[dom]
     return {"bound": d["bound"], "achieved": d["achieved"], "peak": d["peak"], "unit": d["unit"],
-            "frac": d["frac"], "traffic": measured_traffic(dom, w.name), "kernel": dom,
+            "frac": d["frac"], "traffic": measured_traffic(dom, w.name) if profiled else None,
+            "kernel": dom,
             "avg_ms": d["avg_ms"], "source": KERNEL_SOURCE[dom]}
 
 
@@ -262,10 +267,12 @@ def tau_at(t, T):
     return 1.0 + (0.05 - 1.0) * t / (T - 1)
 
 
-def short_run(name, dev, steps=10, warmup=3):
-    """A short run of another workload (same schedule, fused next sample, loss every step):
-    steps/s over ``steps`` timed steps after ``warmup``, then the kernel rooflines of the next
-    ``steps`` steps, each launch between the library's HIP events on its stream."""
+def short_run(name, dev, steps=10, warmup=3, opt=None, samples=1):
+    """A short run of a workload (same schedule, fused next sample, loss every step; Adam unless
+    ``opt`` gives other step parameters, ``samples`` draws per step): steps/s over ``steps``
+    timed steps after ``warmup``, then the kernel rooflines of the next ``steps`` steps, each
+    launch between the library's HIP events on its stream.  The measured traffic of the
+    committed PMC passes is attached only to runs in their configuration (Adam, one sample)."""
     import torch
     from paper_2604_18556_amd import binding as B
     from paper_2604_18556_amd import inputs
@@ -276,10 +283,13 @@ def short_run(name, dev, steps=10, warmup=3):
     del W, Wd, Hd
     loss = torch.zeros(w.batch, device=dev)
 
+    opt = opt or {}
+
     def run(t0, n):
         for t in range(t0, t0 + n):
             layer.step(B.StepParams(tau=tau_at(t, w.steps), lr_scales=w.lr_scales,
-                                    tau_next=tau_at(t + 1, w.steps)), loss_out=loss)
+                                    tau_next=tau_at(t + 1, w.steps), samples=samples, **opt),
+                       loss_out=loss)
     run(0, warmup)
     torch.cuda.synchronize()
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -294,13 +304,19 @@ def short_run(name, dev, steps=10, warmup=3):
     kern = layer.timing_read(reset=True)
     layer.check()
     layer.destroy()
-    per_kernel = kernel_table(kern, algorithmic_work(w, True, True, w.lr_scales), w, steps)
+    lion = opt.get("optimizer") == B.OPT_LION
+    per_kernel = kernel_table(kern, algorithmic_work(w, True, True, w.lr_scales, lion, samples), w, steps)
     out = {"workload": name, "value": 1e3 / ms_step, "unit": "steps/s", "ms_per_step": ms_step,
-           "steps": steps, "warmup": warmup}
-    for k in ("contract", "backward"):
+           "steps": steps, "warmup": warmup, "optimizer": "lion" if lion else "adam",
+           "samples_per_step": samples}
+    profiled = not lion and samples == 1
+    for k in ("forward", "contract", "backward"):
+        if k not in per_kernel:
+            continue
         e = per_kernel[k]
-        out[k] = {key: e[key] for key in ("avg_ms", "bound", "achieved", "peak", "unit", "frac")}
-        out[k]["traffic"] = measured_traffic(k, name)
+        out[k] = {key: e[key] for key in ("avg_ms", "ms_per_step", "bound", "achieved", "peak", "unit",
+                                          "frac")}
+        out[k]["traffic"] = measured_traffic(k, name) if profiled else None
     return out
 
 
@@ -327,6 +343,9 @@ def main():
     ap.add_argument("--variant", default=None,
                     help="workload of a second short run reported under local_shift_variant "
                          "(default: the local-shift form of the default MoE workload; '' skips it)")
+    ap.add_argument("--no-side-runs", action="store_true",
+                    help="skip the short Lion and two-sample runs of the default workload "
+                         "(lion_variant, multi_sample_variant)")
     ap.add_argument("--optimizer", choices=("adam", "lion"), default="adam",
                     help="adam (default) or lion (the paper's optimiser; lr 1e-4, weight decay 1.0)")
     ap.add_argument("--samples", type=int, default=1,
@@ -366,7 +385,8 @@ def main():
     T = w.steps
     fused = not args.no_fuse
     lion = args.optimizer == "lion"
-    opt_kw = dict(optimizer=B.OPT_LION, lr_logits=1e-4, weight_decay=1.0) if lion else {}
+    lion_kw = dict(optimizer=B.OPT_LION, lr_logits=1e-4, weight_decay=1.0)   # Tab. 7's Lion
+    opt_kw = lion_kw if lion else {}
     loss = torch.zeros(w.batch, device=dev)
 
     def run(t0, n):
@@ -418,7 +438,8 @@ def main():
 
     work = algorithmic_work(w, fused, args.loss_every == 1, w.lr_scales, lion, args.samples)
     per_kernel = kernel_table(kern, work, w, args.steps)
-    roofline = dominant_roofline(per_kernel, w)
+    roofline = dominant_roofline(per_kernel, w, profiled=not lion and args.samples == 1 and fused
+                                 and args.loss_every == 1)
 
     # the step's ideal time: each kernel's algorithmic bytes at the HBM peak, or flops at the
     # matrix-core peak, added (the kernels run one after another)
@@ -451,6 +472,15 @@ def main():
         variant["note"] = ("the same experts with the local-shift relaxation (5 logits over "
                            "shifts of the round-to-nearest index), App. E's procedure for "
                            "K-quant sets of more than four values")
+    lion_run = multi = None
+    if w.name == DEFAULT_WORKLOAD and not args.no_side_runs and not lion and args.samples == 1:
+        lion_run = short_run(w.name, dev, opt=lion_kw)
+        lion_run["note"] = ("the same workload under Lion, the paper's optimiser (Tab. 7: lr 1e-4, "
+                            "weight decay 1.0): one moment, 16 instead of 24 state bytes per logit")
+        multi = short_run(w.name, dev, samples=2)
+        multi["note"] = ("the same workload with two independent noise draws per step, gradients "
+                         "and loss averaged (gradient accumulation over resampled noise, §3.3): a "
+                         "second sample pass and contraction, and the backward reads both G")
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -499,6 +529,8 @@ def main():
         "library_gemm": lib_gemm,
         "target_layer": target,
         "local_shift_variant": variant,
+        "lion_variant": lion_run,
+        "multi_sample_variant": multi,
         "gpu_vs_cpu": None if cpu is None else (1e3 / ms_step) / cpu["value"],
     }
     print(json.dumps(out), flush=True)
