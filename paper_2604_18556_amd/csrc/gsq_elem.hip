@@ -376,6 +376,30 @@ constexpr bool backward_plane_update() {
   return kMode == GSQ_RELAX_GRID && K >= 5 && K <= 7;
 }
 
+// Moments staged in LDS: the moment planes of a row go from HBM straight into a per-wavefront
+// LDS area (global_load_lds, no registers held) right after the logits, W and G are requested,
+// so their latency passes during the sample arithmetic; after the sample loop each plane is
+// read back from LDS.  LDS per workgroup: 4 wavefronts x (K or 2K planes) x 1 KB.  Used where
+// it measured faster: Lion over an 8-level grid, whose kernel then holds 150 instead of 184
+// registers and runs three wavefronts per SIMD (4096 x 14336: 1.55 -> 1.45 ms; the MoE experts:
+// 23.7 -> 22.5 ms).  Under Adam the 8-level kernel stays at two wavefronts (its 64 KB of LDS
+// per workgroup) and staging was 0-5 % slower, as it was for the smaller grids, the local shift
+// and the ternary pairs under either optimiser (1-4 %).
+template <int K, int kMode, bool kLion>
+constexpr bool backward_stage_moments() {
+  return kLion && kMode == GSQ_RELAX_GRID && K == 8;
+}
+constexpr int kAuxNT = 2;   // cache policy of a global_load_lds: non-temporal
+
+// Wait until every vector-memory load of this wavefront has landed (the staged moments),
+// leaving the LDS and scalar counters alone; the fences keep the compiler from moving memory
+// accesses across the wait.
+__device__ __forceinline__ void wait_all_vm_loads() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));   // vmcnt(0)
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
 template <int K, bool kF64, bool kScales, bool kMulti, int kMode, bool kLion>
 __global__ __launch_bounds__(kBlock) void k_backward(
     ElemArgs a) {
@@ -383,6 +407,11 @@ __global__ __launch_bounds__(kBlock) void k_backward(
   constexpr int Z = noise_count<K, kMode>();
   __shared__ __align__(16) float win[kMode == GSQ_RELAX_SHIFT ? GSQ_MAX_LEVELS * kWinRow : 4];
   if constexpr (kMode == GSQ_RELAX_SHIFT) fill_windows(win, a);
+  constexpr bool kStage = backward_stage_moments<K, kMode, kLion>();
+  constexpr int kStagePlanes = kLion ? K : 2 * K;   // m (and v) planes of one row
+  __shared__ __align__(16) float4 stage[kStage ? (kBlock / 64) * kStagePlanes * 64 : 1];
+  float4* const sw = stage + (kStage ? __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)) *
+                                           (kStagePlanes * 64) : 0);
   const int lane = threadIdx.x & 63;
   const int64_t col0 = (int64_t)blockIdx.x * kCols + lane * 4;
   const bool active = col0 < a.I;
@@ -412,6 +441,20 @@ __global__ __launch_bounds__(kBlock) void k_backward(
     const uint32_t j4 = chunk_bases<kMode>(a, e0);
     float w[4] = {0.f, 0.f, 0.f, 0.f};
     if (active && (a.want_loss || a.fuse)) load_w4(a.W, a.w_bf16, e0, w);
+    // the first sample's G before the staged moments: loads complete in issue order, so the
+    // sample loop then waits only for the loads it uses
+    const float4 gv0 = active ? ld_stream(a.G + gidx) : make_float4(0.f, 0.f, 0.f, 0.f);
+    if constexpr (kStage) {
+      if (active) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          const int64_t o = state_off(e0, k, K);
+          __builtin_amdgcn_global_load_lds(a.M + o, sw + k * 64, 16, 0, kAuxNT);
+          if constexpr (!kLion)
+            __builtin_amdgcn_global_load_lds(a.V + o, sw + (K + k) * 64, 16, 0, kAuxNT);
+        }
+      }
+    }
     T lacc = 0;   // sum of R G over the thread's coordinates and samples
     // gradient, averaged over the step's independent samples (one unless kMulti)
     T ds_part = 0;
@@ -422,8 +465,9 @@ __global__ __launch_bounds__(kBlock) void k_backward(
       for (int k = 0; k < K; ++k) dacc[q][k] = 0;
     const int M = kMulti ? a.samples : 1;
     for (int smp = 0; smp < M; ++smp) {
-      const float4 gv = active ? ld_stream(a.G + smp * a.g_stride + gidx)
-                               : make_float4(0.f, 0.f, 0.f, 0.f);
+      const float4 gv = smp == 0 ? gv0
+                        : active ? ld_stream(a.G + smp * a.g_stride + gidx)
+                                 : make_float4(0.f, 0.f, 0.f, 0.f);
       float g[4][Z];
       chunk_noise<Z, kF64, kMode>(g, a, (uint64_t)e0, a.t, (uint32_t)smp);
 #pragma unroll
@@ -461,13 +505,19 @@ __global__ __launch_bounds__(kBlock) void k_backward(
     }
     // the moments are needed only by the update: loading them here keeps them out of the
     // registers of the sample loop
-    if constexpr (backward_plane_update<K, kMode>()) {
+    if constexpr (kStage || backward_plane_update<K, kMode>()) {
+      if constexpr (kStage) wait_all_vm_loads();
 #pragma unroll
       for (int k = 0; k < K; ++k) {
-        float4 mk = active ? ld_stream(a.M + state_off(e0, k, K))
-                           : make_float4(0.f, 0.f, 0.f, 0.f);
-        float4 vk = (active && !lion) ? ld_stream(a.V + state_off(e0, k, K))
-                                      : make_float4(0.f, 0.f, 0.f, 0.f);
+        float4 mk, vk = make_float4(0.f, 0.f, 0.f, 0.f);
+        if constexpr (kStage) {
+          mk = active ? sw[k * 64 + lane] : make_float4(0.f, 0.f, 0.f, 0.f);
+          if constexpr (!kLion)
+            vk = active ? sw[(K + k) * 64 + lane] : make_float4(0.f, 0.f, 0.f, 0.f);
+        } else {
+          mk = active ? ld_stream(a.M + state_off(e0, k, K)) : make_float4(0.f, 0.f, 0.f, 0.f);
+          if (active && !lion) vk = ld_stream(a.V + state_off(e0, k, K));
+        }
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           T th = (T)f4get(lv[k], q), m1 = (T)f4get(mk, q), v1 = (T)f4get(vk, q);

@@ -370,6 +370,9 @@ def test_full_size_layer_on_sampled_rows(dev, name):
 FULL_SIZE_VARIANTS = [
     ("attn-4096x4096-k3", dict(optimizer=B.OPT_LION, lr_logits=1e-4, weight_decay=1.0)),
     ("mlp-down-4096x14336-shift8", dict(optimizer=B.OPT_LION, lr_logits=1e-4, weight_decay=1.0)),
+    # the 8-level grid under Lion stages its moments in LDS: trained and frozen (super-block) scales
+    ("mlp-down-4096x14336-k8", dict(optimizer=B.OPT_LION, lr_logits=1e-4, weight_decay=1.0)),
+    ("moe-64x2048x7168-superblock", dict(optimizer=B.OPT_LION, lr_logits=1e-4, weight_decay=1.0)),
     ("attn-4096x4096-ternary", dict(samples=3)),
     ("mlp-up-14336x4096-k8", dict(samples=2)),
 ]
