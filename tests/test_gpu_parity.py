@@ -375,6 +375,7 @@ FULL_SIZE_VARIANTS = [
     ("moe-64x2048x7168-superblock", dict(optimizer=B.OPT_LION, lr_logits=1e-4, weight_decay=1.0)),
     ("attn-4096x4096-ternary", dict(samples=3)),
     ("mlp-up-14336x4096-k8", dict(samples=2)),
+    ("moe-64x2048x7168-superblock", dict(samples=2)),
 ]
 
 
