@@ -383,8 +383,8 @@ constexpr bool backward_plane_update() {
 // it measured faster: Lion over an 8-level grid, whose kernel then holds 150 instead of 184
 // registers and runs three wavefronts per SIMD (4096 x 14336: 1.55 -> 1.45 ms; the MoE experts:
 // 23.7 -> 22.5 ms).  Under Adam the 8-level kernel stays at two wavefronts (its 64 KB of LDS
-// per workgroup) and staging was 0-5 % slower (1.5-4.5 % with two draws per step), as it was
-// for the smaller grids, the local shift and the ternary pairs under either optimiser (1-4 %).
+// per workgroup) and staging was 0-5 % slower, as it was for the smaller grids, the local shift
+// and the ternary pairs under either optimiser (1-4 %).
 template <int K, int kMode, bool kLion>
 constexpr bool backward_stage_moments() {
   return kLion && kMode == GSQ_RELAX_GRID && K == 8;
