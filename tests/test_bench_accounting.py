@@ -149,3 +149,18 @@ def test_mfma_summary_arithmetic(tmp_path, capsys):
     assert float(step[7]) == pytest.approx(gflop / 100e-6 / 1e3, abs=1)      # TFLOP/s
     # hard-loss row: "contract hard loss n us ..." has one more token before the numbers
     assert float(hard[6]) == pytest.approx(0.25) and float(hard[5]) == pytest.approx(2.0)
+
+
+def test_measured_traffic_only_for_the_profiled_configuration():
+    """The roofline's traffic comes from PMC passes of the Adam, one-draw, fused, loss-every-step
+    run; any other configuration (Lion, several draws) reports it as null."""
+    b = _bench()
+    w = inputs.WORKLOADS["moe-64x2048x7168-superblock"]
+    per_kernel = {"backward": {"bound": "hbm", "achieved": 6000.0, "peak": 8000.0, "unit": "GB/s",
+                               "frac": 0.75, "avg_ms": 30.0, "ms_per_step": 30.0},
+                  "contract": {"bound": "mfma", "achieved": 1200.0, "peak": 2500.0, "unit": "TFLOP/s",
+                               "frac": 0.48, "avg_ms": 11.0, "ms_per_step": 11.0}}
+    r = b.dominant_roofline(per_kernel, w, profiled=False)
+    assert r["kernel"] == "backward" and r["traffic"] is None
+    r = b.dominant_roofline(per_kernel, w, profiled=True)
+    assert r["traffic"] == b.measured_traffic("backward", w.name)
