@@ -533,6 +533,66 @@ def _check_full_size_harden_and_pack(dev, layer, w, pair_cfg, rcfg, st, gst, exp
                                       ref.scales_fp16(gst.scales))
 
 
+# ------------------------------------------------------------------ rows beyond one grid pass
+ROWS_PER_PASS = 65535 * 4   # the elementwise kernels' grid: 65535 blocks of 4 rows, then a loop
+
+
+@pytest.mark.parametrize("opt", ["adam", "lion"])
+def test_rows_beyond_one_pass_of_the_row_grid(dev, opt):
+    """The elementwise kernels cover at most 65535 x 4 rows per pass of their grid and loop over
+    the rest.  A 262400 x 256 layer (8 levels, trained scales) steps twice (next sample fused,
+    loss requested) and hardens; rows on both sides of the pass boundary, among them rows that
+    one wavefront handles in both passes (3 and 262143), must match the oracle.  Under Lion the
+    8-level backward stages its moments in LDS, which the second pass reuses."""
+    O, I, K, gs = ROWS_PER_PASS + 260, 256, 8, 128
+    W, H = layer_inputs(O, I)
+    rows = np.array([0, 3, ROWS_PER_PASS - 1, ROWS_PER_PASS, ROWS_PER_PASS + 3, O - 1])
+    rcfg = ref.Config(O, I, L8, gs, precision="bf16", seed=5)
+    cfg = B.LayerConfig(O, I, L8, gs, precision=B.PREC_BF16, seed=5)
+    print(f"[rows beyond one pass] {opt} O={O} I={I}", flush=True)
+    layer = B.Layer(cfg, torch.from_numpy(W).to(dev).to(torch.bfloat16),
+                    torch.from_numpy(H).to(dev))
+    Hs = ref.symmetrize(H)
+    st = ref.init_layer(rcfg, W, rows=rows)
+    opt_kw = dict(optimizer=B.OPT_LION, lr_logits=1e-4, weight_decay=1.0) if opt == "lion" else {}
+    buf = torch.empty(1, O, I, K, device=dev)
+    sbuf = torch.empty(1, O, I // gs, device=dev)
+
+    def planes(**which):
+        ((key, out),) = which.items()
+        t = layer.get_state(**{key: out})
+        return out[:, rows].cpu().numpy(), t
+
+    lg, _ = planes(logits=buf)
+    assert rel_err(lg, st.logits) <= 1e-6
+    for t in range(2):
+        tau, nxt = ref.tau_schedule(t, 100), ref.tau_schedule(t + 1, 100)
+        prm = B.StepParams(tau=tau, tau_next=nxt, **opt_kw)
+        loss = torch.zeros(1, device=dev)
+        layer.step(prm, loss_out=loss)
+        G = torch.empty(1, O, I, device=dev)
+        layer.intermediates(grad=G)
+        G_rows = G[:, rows].cpu().numpy()
+        del G
+        st_new, _, inter = ref.step(rcfg, W, Hs, st, oracle_params(prm), rows=rows, want=True)
+        assert rel_err(G_rows, inter["G"]) <= 1e-3, (t, rel_err(G_rows, inter["G"]))
+        got = {}
+        for key in ("logits", "m", "v"):
+            got[key], tt = planes(**{key: buf})
+        for key in ("scales", "m_s", "v_s"):
+            got[key], _ = planes(**{key: sbuf})
+        gst = ref.State(*(got[k] for k in ("logits", "m", "v", "scales", "m_s", "v_s")), tt)
+        assert_state_close(gst, st_new, inter["G"], 1e-3, t + 1, label=f"{opt} step {t}",
+                           dlogits=inter["dlogits"])
+        assert np.isfinite(loss.item()) and loss.item() > 0
+        st = st_new
+    codes = torch.empty(1, O, I, dtype=torch.uint8, device=dev)
+    layer.harden(codes=codes)
+    np.testing.assert_array_equal(codes[:, rows].cpu().numpy(), ref.harden(gst.logits))
+    layer.check()
+    layer.destroy()
+
+
 # ------------------------------------------------------------------ Lion (§3.3) and AdamW (App. B)
 @pytest.mark.parametrize("opt", ["lion", "adamw"])
 @pytest.mark.parametrize("prec,O,I,K,gs,tau", [("fp32", 256, 256, 4, 128, 0.2),
