@@ -43,7 +43,7 @@ ONCE_REPS = 5                  # timed calls of gsq_harden / gsq_pack
 
 
 def algorithmic_work(w, fused, want_loss, lr_scales, lion=False, samples=1):
-    """Per-launch algorithmic bytes / flops of each step kernel (see the design notes).
+    """Per-launch algorithmic bytes / flops of each step kernel.
 
     Per coordinate, bf16 W and R, fp32 logits / moments / gradient, K levels, groups of gs:
       forward   4K (logits) + 2 (W) + 2 (R)                      + 4/gs (scale)

@@ -25,8 +25,8 @@ Three relaxations of a coordinate's choice (``Config.relaxation``):
 * "ternary": the mask x sign form of §3.1 (Eq. 2, Alg. 2), two binary
   relaxations per coordinate with logits {-l, l} each.
 
-Readings where the paper is silent are listed in the design notes; each is
-repeated at the function that takes it.
+Where the paper is silent, the reading taken is stated at the function that
+takes it.
 """
 from dataclasses import dataclass, field
 
