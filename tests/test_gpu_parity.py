@@ -376,6 +376,9 @@ FULL_SIZE_VARIANTS = [
     ("attn-4096x4096-ternary", dict(samples=3)),
     ("mlp-up-14336x4096-k8", dict(samples=2)),
     ("moe-64x2048x7168-superblock", dict(samples=2)),
+    # the other pairings of the relaxations with Lion and several draws
+    ("attn-4096x4096-ternary", dict(optimizer=B.OPT_LION, lr_logits=1e-4, weight_decay=1.0)),
+    ("mlp-down-4096x14336-shift8", dict(samples=2)),
 ]
 
 
