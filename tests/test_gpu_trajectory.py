@@ -62,7 +62,8 @@ def near_ties(rcfg, logits):
 # Lion (the paper's optimiser, Tab. 7's lr 1e-4 and weight decay 1.0) over whole runs too
 LION = dict(optimizer=B.OPT_LION, lr_logits=1e-4, weight_decay=1.0)
 CASES = [(n, {}) for n in RUNS] + [("attn-4096x4096-k3", LION),
-                                   ("mlp-down-4096x14336-shift8", LION)]
+                                   ("mlp-down-4096x14336-shift8", LION),
+                                   ("moe-64x2048x7168-superblock", LION)]
 
 
 @pytest.mark.timeout(900)
@@ -161,14 +162,25 @@ def test_full_run_on_sampled_rows(dev, name, opt):
     # the drift of its own logits (the oracle's top-2 gap below their summed differences),
     # differing codes and drifting logits must stay rare, and no logit can drift more than
     # 2 lr per step.
+    # Logits far below their coordinate's top (kappa times the gap over the run's largest tau
+    # beyond -ln(FLT_MIN) = 87.3, e.g. the far levels of an 8-level grid under App. A's prior)
+    # have a softmax weight below fp32's normal range at every step: the kernel's fp32 gradient
+    # there is 0 or a denormal of a few bits, so Lion moves them by weight decay alone or by
+    # steps of an unreliable sign, while the oracle's float64 weight is tiny but exact and
+    # Lion's sign makes a full step of it every step. Those are counted apart; the bound on
+    # drifting logits applies to all others.
     lr = opt["lr_logits"]
     d = np.abs(lg.astype(np.float64) - st.logits)
-    far = np.mean(d > 4 * lr)
-    srt = np.sort(np.asarray(st.logits, np.float64), -1)
+    L64 = np.asarray(st.logits, np.float64)
+    underflow = (L64.max(-1, keepdims=True) - L64) * 1.0 / ref.tau_schedule(0, T) > 87.3  # kappa 1
+    far = np.mean((d > 4 * lr) & ~underflow)
+    far_u = np.mean((d > 4 * lr) & underflow)
+    srt = np.sort(L64, -1)
     gap = srt[..., -1] - srt[..., -2]
     ds = np.abs(sc.astype(np.float64) - st.scales)
     far_s = np.mean(ds > 4 * w.lr_scales)
-    print(f"  Lion: {far:.2e} of logits beyond 4 lr, max drift {d.max():.2e}; "
+    print(f"  Lion: {far:.2e} of logits beyond 4 lr ({far_u:.2e} more where the fp32 weight "
+          f"underflows, {underflow.mean():.2e} of all), max drift {d.max():.2e}; "
           f"{far_s:.2e} of scales beyond 4 lr_scales, max drift {ds.max():.2e}")
     assert far < 1e-2 and diff.mean() < 1e-3 and d.max() <= 2 * lr * T
     # the scales take the same sign steps (lr_scales); there are few of them per sampled row
