@@ -116,6 +116,9 @@ CASES = [
     ("bf16", 1, 40, 384, 7, 128, "group", 0.1, 1.0),
     ("fp32", 1, 24, 256, 6, 64, "group", 0.3, 1.0),
     ("fp32", 1, 24, 256, 8, 128, "group", 0.3, 1.0),
+    # groups of 256: one scale per wavefront row, its gradient summed over all 64 lanes
+    ("bf16", 1, 50, 512, 4, 256, "group", 0.3, 1.0),
+    ("fp32", 2, 20, 768, 3, 256, "group", 0.5, 1.0),
     # more than one chunk (2048 row partials) of the loss reduction per layer: 2304 and
     # 3 x 2000 partials, so the fixed-order chunk sums and the last-block hand-off are exercised
     ("fp32", 1, 2304, 256, 4, 128, "group", 0.3, 1.0),
@@ -161,9 +164,9 @@ def test_single_step_matches_oracle(dev, prec, batch, O, I, K, gs, layout, tau, 
 # ------------------------------------------------------------------ harden / pack
 @pytest.mark.parametrize("K,gs,layout", [(4, 128, "group"), (3, 64, "group"), (8, 128, "group"),
                                          (2, 16, "group"), (5, 64, "group"), (7, 32, "group"),
-                                         (8, 16, "superblock")])
+                                         (6, 256, "group"), (8, 16, "superblock")])
 def test_harden_and_pack_are_bit_exact(dev, K, gs, layout):
-    levels = {2: L2, 3: L3, 4: L4, 5: L5, 7: L7, 8: L8}[K]
+    levels = {2: L2, 3: L3, 4: L4, 5: L5, 6: L6, 7: L7, 8: L8}[K]
     O, I, batch = 37, 512, 2
     W, H = layer_inputs(O, I, batch=batch, seed=K)
     rcfg = ref.Config(O, I, levels, gs, batch=batch, layout=layout, precision="bf16", seed=2)
