@@ -57,7 +57,7 @@ def configs(rcfg):
 class Pair:
     """A GPU layer and the oracle state it mirrors."""
 
-    def __init__(self, rcfg, W, H, dev):
+    def __init__(self, rcfg, W, H, dev, scales_init=None):
         import torch
         self.torch = torch
         self.dev = dev
@@ -67,7 +67,10 @@ class Pair:
         wt = torch.from_numpy(self.W).to(dev)
         if rcfg.precision == "bf16":
             wt = wt.to(torch.bfloat16)
-        self.layer = B.Layer(self.bcfg, wt, torch.from_numpy(self.H).to(dev))
+        s0 = None
+        if scales_init is not None:
+            s0 = torch.from_numpy(np.ascontiguousarray(scales_init, np.float32)).to(dev)
+        self.layer = B.Layer(self.bcfg, wt, torch.from_numpy(self.H).to(dev), scales_init=s0)
         self.Hs = ref.symmetrize(self.H)
 
     # -- state transfer

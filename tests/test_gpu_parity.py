@@ -86,6 +86,35 @@ def test_init_matches_oracle(dev, prec, O, I, K, gs):
     np.testing.assert_array_equal(codes.cpu().numpy(), ref.init_layer(rcfg0, W).extra["q0"])
 
 
+@pytest.mark.parametrize("prec", ["fp32", "bf16"])
+def test_init_from_given_scales_and_a_step(dev, prec):
+    """Initial scales supplied by the caller (scales_init, e.g. those of a GPTQ warm start, which
+    round-to-nearest absmax scales stand in for otherwise, Eq. 4's paragraph): the library keeps
+    them as given, derives the round-to-nearest codes and the logits from them, and steps from
+    there like the oracle started from the same scales."""
+    O, I, gs = 70, 384, 64
+    W, H = layer_inputs(O, I, bf16=prec == "bf16", seed=21)
+    rcfg = ref.Config(O, I, L4, gs, precision=prec, seed=9)
+    rng = np.random.default_rng(21)
+    s0 = (ref.init_layer(rcfg, W).scales * rng.uniform(0.6, 1.5, (1, O, I // gs))).astype(np.float32)
+    pair = Pair(rcfg, W, H, dev, scales_init=s0)
+    st = ref.init_layer(rcfg, W, scales_init=s0)
+    got = pair.get()
+    np.testing.assert_array_equal(got.scales, s0)
+    assert rel_err(got.logits, st.logits) <= 1e-6
+    rcfg0 = ref.Config(O, I, L4, gs, precision=prec, init_noise=False)
+    pair0 = Pair(rcfg0, W, H, dev, scales_init=s0)
+    codes = torch.empty(1, O, I, dtype=torch.uint8, device=dev)
+    pair0.layer.harden(codes=codes)
+    np.testing.assert_array_equal(codes.cpu().numpy(), ref.init_layer(rcfg0, W, scales_init=s0).extra["q0"])
+    prm = B.StepParams(tau=0.4)
+    loss = pair.step(prm)
+    new, L, inter = ref.step(rcfg, W, pair.Hs, st, oracle_params(prm), want=True)
+    tol = TOL[prec]
+    assert np.all(np.abs(loss - L) <= tol * np.abs(L)), (loss, L)
+    assert_state_close(pair.get(), new, inter["G"], tol, 1, label=f"given scales {prec}")
+
+
 def test_superblock_init_matches_oracle(dev):
     W, H = layer_inputs(48, 512, batch=3, seed=5)
     W[0, 0, :16] = 0.0
