@@ -366,6 +366,33 @@ def test_non_finite_gradients_are_reported_without_a_loss(dev, opt):
     assert e.value.status == B.GSQ_ENONFINITE
 
 
+def test_intermediates_belong_to_the_last_step(dev):
+    """gsq_get_intermediates returns the last step's R and G, and refuses (GSQ_EINVAL) when no
+    step has run since init, set_state, or a harden whose hard loss reused the G buffer."""
+    W, H = layer_inputs(40, 256, seed=6)
+    rcfg = ref.Config(40, 256, L4, 128, precision="bf16", seed=2)
+    pair = Pair(rcfg, W, H, dev)
+
+    def refused():
+        with pytest.raises(B.GsqError) as e:
+            pair.intermediates()
+        return e.value.status == B.GSQ_EINVAL
+
+    assert refused()
+    st = ref.init_layer(rcfg, W)
+    pair.step(B.StepParams(tau=0.5))
+    R, G = pair.intermediates()
+    _, _, inter = ref.step(rcfg, W, pair.Hs, st, oracle_params(B.StepParams(tau=0.5)), want=True)
+    assert rel_err(G, inter["G"]) <= 1e-3
+    hl = torch.zeros(1, device=dev)
+    pair.layer.harden(hard_loss=hl)
+    assert refused()
+    pair.step(B.StepParams(tau=0.4))
+    pair.intermediates()
+    pair.put(pair.get())
+    assert refused()
+
+
 def test_superblock_rejects_scale_training(dev):
     W, H = layer_inputs(16, 256, seed=2)
     rcfg = ref.Config(16, 256, L8, layout="superblock", precision="bf16")
